@@ -1,0 +1,163 @@
+/*
+ * greencache.h - C ABI of the MI355X (gfx950) prefix-cached prefill path.
+ *
+ * GreenCache (arXiv 2505.23970) keeps the KV of earlier requests' context and
+ * reuses it: when a request's context prefix is found in the cache, the
+ * cached tokens' KV is joined with the new tokens' KV and both are processed
+ * together, and the new tokens' KV is saved for later requests (§2.2
+ * "Caching for LLM Serving", Fig. 1a, steps 1 and 2). This library is that
+ * step on one GPU: it appends the new (suffix) tokens' K/V into a paged KV
+ * pool and runs causal attention of the new tokens' queries over the cached
+ * prefix plus the new tokens. Cache lookup, token matching, eviction and
+ * sizing belong to the caller (the paper's cache manager, §5.5).
+ *
+ * Attention computed (the paper states no formula; textbook causal scaled
+ * dot-product attention with grouped KV heads, §2.1 prefill): for new token i
+ * of request r at logical position P_r + i and query head h, with
+ * kvh = h / (Hq / Hkv),
+ *     o = sum_{j <= P_r + i} softmax_j(scale * <q, k_j>) * v_j,
+ *     lse = ln sum_{j <= P_r + i} exp(scale * <q, k_j>).
+ *
+ * Conventions shared by every entry point
+ *   - All buffers belong to the caller. The library allocates no device or
+ *     host memory and keeps no mutable global state; entry points are
+ *     thread-safe. Work is enqueued on `stream` and the call returns without
+ *     waiting; host arrays are only read during the call, device arrays must
+ *     stay alive until the stream has run the work.
+ *   - bf16 tensors are passed as pointers to IEEE bfloat16 bit patterns.
+ *   - Packed new tokens: row t of q / k_new / v_new / out is new token
+ *     t - cu_r of request r, where cu_r = new_lens[0] + ... + new_lens[r-1].
+ *     T = sum of new_lens.
+ *   - Pool layout (value pages are stored transposed so that the attention
+ *     kernel reads both operands of its matrix products with 16-byte loads):
+ *       k_pool  bf16 [num_blocks][num_kv_heads][page_size][head_dim]
+ *       v_pool  bf16 [num_blocks][num_kv_heads][head_dim][page_size]
+ *     Logical key j of request r lives in block block_tables[r][j / page_size],
+ *     slot j % page_size.
+ *   - Supported: head_dim 64 or 128; page_size 16; num_q_heads a multiple of
+ *     num_kv_heads with num_q_heads / num_kv_heads <= 128.
+ *   - Errors detectable on the host are returned before anything is enqueued
+ *     and leave every buffer untouched. A block id outside [0, num_blocks) in
+ *     a table entry the batch needs is not checked on the host: the kernels
+ *     skip such pages (append writes nothing there; attention reads zeros),
+ *     so a bad id never causes an out-of-bounds access, but the result is
+ *     then undefined. Two requests appending into the same slot race.
+ *     GC_ERR_HIP reports a failed launch; the HIP error is not cleared.
+ *   - batch == 0 or T == 0: GC_OK, nothing is enqueued.
+ */
+#ifndef GREENCACHE_H
+#define GREENCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gc_status {
+    GC_OK = 0,
+    GC_ERR_NULL_ARG = -1,    /* a required pointer is NULL */
+    GC_ERR_BAD_SHAPE = -2,   /* negative length, Hq % Hkv != 0, non-positive sizes, bad scale */
+    GC_ERR_UNSUPPORTED = -3, /* head_dim not 64/128, page_size != 16, Hq/Hkv > 128 */
+    GC_ERR_BLOCK_TABLE = -4, /* ceil((P_r + n_r) / page_size) > max_blocks_per_seq */
+    GC_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required */
+    GC_ERR_HIP = -6          /* a HIP launch or runtime call failed */
+} gc_status;
+
+/* Model and pool geometry. */
+typedef struct gc_geometry {
+    int32_t num_q_heads;        /* Hq */
+    int32_t num_kv_heads;       /* Hkv */
+    int32_t head_dim;           /* D */
+    int32_t page_size;          /* keys per pool block (16) */
+    int32_t num_blocks;         /* blocks in each pool */
+    int32_t max_blocks_per_seq; /* row length of block_tables */
+} gc_geometry;
+
+/* One ragged batch of requests whose prefixes hit the cache (P_r may be 0: a
+ * miss is a plain causal prefill). Host and device copies of the lengths
+ * must hold the same values. */
+typedef struct gc_batch {
+    int32_t batch;                   /* B >= 0 */
+    const int32_t* prefix_lens_host; /* [B] cached tokens already in the pool, P_r >= 0 */
+    const int32_t* new_lens_host;    /* [B] new tokens, n_r >= 0 */
+    const int32_t* prefix_lens_dev;  /* [B] device copy of prefix_lens_host */
+    const int32_t* cu_new_lens_dev;  /* [B+1] device: 0, n_0, n_0+n_1, ..., T */
+    const int32_t* block_tables_dev; /* [B][max_blocks_per_seq] device, physical block ids */
+} gc_batch;
+
+/* Work-split options of the attention call. Pass NULL for the defaults. */
+typedef struct gc_plan_options {
+    /* 0: automatic. > 0: split the keys of every query tile into chunks of this
+     * many 64-key tiles, merged by log-sum-exp. < 0: never split. */
+    int32_t kv_split_tiles;
+    int32_t reserved[7];     /* must be zero */
+} gc_plan_options;
+
+/*
+ * Save the new tokens' K/V into the pool (§2.2, step 1: the processed
+ * request's KV is stored for reuse). For every request r, new token i and KV
+ * head h, the head_dim values of k_new[cu_r + i][h] and v_new[cu_r + i][h] are
+ * copied bit for bit to slot (P_r + i) % page_size of block
+ * block_tables[r][(P_r + i) / page_size]. No other pool byte changes.
+ *   k_new, v_new : device bf16 [T][Hkv][D]
+ *   k_pool, v_pool: device bf16 pools (layout above), updated in place
+ * Call it before the attention call, which reads the new tokens' K/V from the
+ * pool.
+ */
+gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch,
+                       const void* k_new, const void* v_new,
+                       void* k_pool, void* v_pool, hipStream_t stream);
+
+/*
+ * Device workspace, in bytes, that the attention call needs for this batch and
+ * these options (work list plus split-KV partial results). Writes *bytes.
+ */
+gc_status gc_prefix_prefill_workspace_size(const gc_geometry* geo, const gc_batch* batch,
+                                           const gc_plan_options* opts, size_t* bytes);
+
+/*
+ * Build the attention work list in `workspace` on the device from the device
+ * length arrays (one small kernel; no host-to-device copy). A plan stays valid
+ * for every later gc_prefix_prefill_run with the same batch and options, so a
+ * serving loop plans once per batch and runs once per layer.
+ */
+gc_status gc_prefix_prefill_plan(const gc_geometry* geo, const gc_batch* batch,
+                                 const gc_plan_options* opts,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Attention of the new tokens over the cached prefix plus the new tokens
+ * (§2.2, step 2), using a plan made by gc_prefix_prefill_plan on the same
+ * stream for the same batch and options.
+ *   q     : device bf16 [T][Hq][D]
+ *   scale : softmax scale, finite and > 0 (callers pass 1/sqrt(D))
+ *   out   : device bf16 [T][Hq][D], rounded to nearest even
+ *   lse   : device fp32 [T][Hq] natural-log log-sum-exp, or NULL
+ * The pools must already hold every key of every request (prefix and new).
+ */
+gc_status gc_prefix_prefill_run(const gc_geometry* geo, const gc_batch* batch,
+                                const gc_plan_options* opts,
+                                const void* q, const void* k_pool, const void* v_pool,
+                                float scale, void* out, float* lse,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* gc_prefix_prefill_plan followed by gc_prefix_prefill_run. */
+gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* batch,
+                                      const gc_plan_options* opts,
+                                      const void* q, const void* k_pool, const void* v_pool,
+                                      float scale, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* gc_status_string(gc_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GREENCACHE_H */

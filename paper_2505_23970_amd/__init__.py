@@ -1,0 +1,276 @@
+"""Prefix-cached prefill attention on MI355X (gfx950): Python binding.
+
+GreenCache (arXiv 2505.23970, §2.2, Fig. 1a) reuses the KV of a request's
+cached context: the new tokens' KV is appended to the cache and the new
+tokens attend over the cached prefix plus themselves. The work runs in the
+HIP library libgreencache.so (C ABI in include/greencache.h); this module
+only checks tensors and marshals pointers, shapes and the current stream.
+PyTorch provides device memory and streams. There is no fallback path: if
+the library is not built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(_HERE, "libgreencache.so")
+
+GC_OK = 0
+STATUS_NAMES = {0: "GC_OK", -1: "GC_ERR_NULL_ARG", -2: "GC_ERR_BAD_SHAPE", -3: "GC_ERR_UNSUPPORTED",
+                -4: "GC_ERR_BLOCK_TABLE", -5: "GC_ERR_WORKSPACE", -6: "GC_ERR_HIP"}
+
+EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefill_plan",
+            "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_status_string")
+
+
+class GcError(RuntimeError):
+    def __init__(self, fn, status, lib=None):
+        text = STATUS_NAMES.get(status, str(status))
+        if lib is not None:
+            try:
+                text = lib.gc_status_string(status).decode()
+            except Exception:
+                pass
+        super().__init__(f"{fn} failed: {text}")
+        self.status = status
+
+
+class Geometry(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int32), ("max_blocks_per_seq", ctypes.c_int32)]
+
+
+class BatchDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32),
+                ("prefix_lens_host", ctypes.POINTER(ctypes.c_int32)),
+                ("new_lens_host", ctypes.POINTER(ctypes.c_int32)),
+                ("prefix_lens_dev", ctypes.c_void_p),
+                ("cu_new_lens_dev", ctypes.c_void_p),
+                ("block_tables_dev", ctypes.c_void_p)]
+
+
+class PlanOptions(ctypes.Structure):
+    _fields_ = [("kv_split_tiles", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+
+
+_lib = None
+
+
+def load_library(path: str | None = None):
+    """Load libgreencache.so. Raises if it has not been built: there is no other path."""
+    global _lib
+    if path is None and _lib is not None:
+        return _lib
+    p = path or LIBRARY
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build it with `python -m paper_2505_23970_amd.build`")
+    lib = ctypes.CDLL(p)
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    G, Bp, O = ctypes.POINTER(Geometry), ctypes.POINTER(BatchDesc), ctypes.POINTER(PlanOptions)
+    lib.gc_kv_append.restype = i32
+    lib.gc_kv_append.argtypes = [G, Bp, vp, vp, vp, vp, vp]
+    lib.gc_prefix_prefill_workspace_size.restype = i32
+    lib.gc_prefix_prefill_workspace_size.argtypes = [G, Bp, O, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gc_prefix_prefill_plan.restype = i32
+    lib.gc_prefix_prefill_plan.argtypes = [G, Bp, O, vp, ctypes.c_size_t, vp]
+    for fn in (lib.gc_prefix_prefill_run, lib.gc_prefix_prefill_attention):
+        fn.restype = i32
+        fn.argtypes = [G, Bp, O, vp, vp, vp, ctypes.c_float, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gc_status_string.restype = ctypes.c_char_p
+    lib.gc_status_string.argtypes = [i32]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(fn, status, lib):
+    if status != GC_OK:
+        raise GcError(fn, status, lib)
+
+
+def _stream_handle(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _require(t, dtype, name, device=None):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on the GPU (got {t.device})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class PagedBatch:
+    """A ragged batch: host lengths (numpy) plus their device copies (torch).
+
+    prefix_lens[r]: cached tokens of request r already in the pool;
+    new_lens[r]: its new tokens; block_tables[r][p]: physical block of logical page p.
+    """
+
+    def __init__(self, prefix_lens, new_lens, block_tables, device="cuda"):
+        import torch
+        self.prefix_lens = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+        self.new_lens = np.ascontiguousarray(new_lens, dtype=np.int32)
+        bt = np.ascontiguousarray(block_tables, dtype=np.int32)
+        if bt.ndim != 2 or bt.shape[0] != self.prefix_lens.shape[0]:
+            raise ValueError("block_tables must be [batch][max_blocks_per_seq]")
+        self.block_tables_host = bt
+        cu = np.zeros(self.prefix_lens.shape[0] + 1, np.int32)
+        np.cumsum(self.new_lens, out=cu[1:])
+        self.cu_new_lens = cu
+        self.device = torch.device(device)
+        self.prefix_lens_dev = torch.from_numpy(self.prefix_lens.copy()).to(self.device)
+        self.cu_new_lens_dev = torch.from_numpy(cu.copy()).to(self.device)
+        self.block_tables_dev = torch.from_numpy(bt.copy()).to(self.device)
+        self._desc = BatchDesc(
+            int(self.prefix_lens.shape[0]),
+            self.prefix_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            self.new_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            self.prefix_lens_dev.data_ptr(), self.cu_new_lens_dev.data_ptr(),
+            self.block_tables_dev.data_ptr())
+
+    @property
+    def batch(self) -> int:
+        return int(self.prefix_lens.shape[0])
+
+    @property
+    def total_new(self) -> int:
+        return int(self.new_lens.sum())
+
+    @property
+    def max_blocks_per_seq(self) -> int:
+        return int(self.block_tables_host.shape[1])
+
+    def desc(self) -> BatchDesc:
+        return self._desc
+
+
+def geometry(num_q_heads, num_kv_heads, head_dim, num_blocks, max_blocks_per_seq, page_size=16):
+    return Geometry(int(num_q_heads), int(num_kv_heads), int(head_dim), int(page_size),
+                    int(num_blocks), int(max_blocks_per_seq))
+
+
+def _geo_from_pools(k_pool, v_pool, q_heads, batch: PagedBatch):
+    NB, Hkv, S, D = k_pool.shape
+    if tuple(v_pool.shape) != (NB, Hkv, D, S):
+        raise ValueError(f"v_pool must be [NB][Hkv][D][S] = {(NB, Hkv, D, S)}, got {tuple(v_pool.shape)}")
+    return geometry(q_heads, Hkv, D, NB, batch.max_blocks_per_seq, S)
+
+
+def _opts(kv_split_tiles):
+    if kv_split_tiles is None:
+        return None
+    o = PlanOptions()
+    o.kv_split_tiles = int(kv_split_tiles)
+    return ctypes.byref(o)
+
+
+def kv_append(k_new, v_new, k_pool, v_pool, batch: PagedBatch, stream=None):
+    """Append the new tokens' K/V ([T][Hkv][D] bf16) into the pools in place."""
+    import torch
+    lib = load_library()
+    for name, t in (("k_new", k_new), ("v_new", v_new), ("k_pool", k_pool), ("v_pool", v_pool)):
+        _require(t, torch.bfloat16, name, batch.device)
+    geo = _geo_from_pools(k_pool, v_pool, k_pool.shape[1], batch)
+    T, Hkv, D = k_new.shape
+    if (T, Hkv, D) != (batch.total_new, geo.num_kv_heads, geo.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [T][Hkv][D] matching the batch and pools")
+    st = lib.gc_kv_append(ctypes.byref(geo), ctypes.byref(batch.desc()), k_new.data_ptr(),
+                          v_new.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
+                          _stream_handle(stream))
+    _check("gc_kv_append", st, lib)
+
+
+def workspace_size(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None) -> int:
+    lib = load_library()
+    geo = _geo_from_pools(k_pool, v_pool, num_q_heads, batch)
+    out = ctypes.c_size_t(0)
+    st = lib.gc_prefix_prefill_workspace_size(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                              _opts(kv_split_tiles), ctypes.byref(out))
+    _check("gc_prefix_prefill_workspace_size", st, lib)
+    return int(out.value)
+
+
+def alloc_workspace(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None):
+    import torch
+    n = workspace_size(num_q_heads, k_pool, v_pool, batch, kv_split_tiles)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=batch.device)
+
+
+def _attn_args(q, k_pool, v_pool, batch, out, lse, workspace):
+    import torch
+    _require(q, torch.bfloat16, "q", batch.device)
+    _require(k_pool, torch.bfloat16, "k_pool", batch.device)
+    _require(v_pool, torch.bfloat16, "v_pool", batch.device)
+    T, Hq, D = q.shape
+    geo = _geo_from_pools(k_pool, v_pool, Hq, batch)
+    if T != batch.total_new or D != geo.head_dim:
+        raise ValueError("q must be [T][Hq][D] matching the batch and pools")
+    if out is None:
+        out = torch.empty_like(q)
+    _require(out, torch.bfloat16, "out", batch.device)
+    if tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must have q's shape")
+    if lse is not None:
+        _require(lse, torch.float32, "lse", batch.device)
+        if tuple(lse.shape) != (T, Hq):
+            raise ValueError("lse must be [T][Hq] float32")
+    _require(workspace, torch.uint8, "workspace", batch.device)
+    return geo, out
+
+
+def plan(num_q_heads, k_pool, v_pool, batch: PagedBatch, workspace, kv_split_tiles=None, stream=None):
+    import torch
+    lib = load_library()
+    _require(workspace, torch.uint8, "workspace", batch.device)
+    geo = _geo_from_pools(k_pool, v_pool, num_q_heads, batch)
+    st = lib.gc_prefix_prefill_plan(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                    _opts(kv_split_tiles), workspace.data_ptr(),
+                                    workspace.numel(), _stream_handle(stream))
+    _check("gc_prefix_prefill_plan", st, lib)
+
+
+def run(q, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=None,
+        kv_split_tiles=None, stream=None):
+    lib = load_library()
+    geo, out = _attn_args(q, k_pool, v_pool, batch, out, lse, workspace)
+    st = lib.gc_prefix_prefill_run(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                   _opts(kv_split_tiles), q.data_ptr(), k_pool.data_ptr(),
+                                   v_pool.data_ptr(), float(scale), out.data_ptr(),
+                                   lse.data_ptr() if lse is not None else None,
+                                   workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    _check("gc_prefix_prefill_run", st, lib)
+    return out
+
+
+def prefix_prefill_attention(q, k_pool, v_pool, batch: PagedBatch, scale, workspace=None,
+                             out=None, lse=None, kv_split_tiles=None, stream=None):
+    """Attention of the new tokens (q: [T][Hq][D] bf16) over cached prefix + new keys.
+
+    The pools must already hold the new tokens' K/V (call kv_append first).
+    Returns out ([T][Hq][D] bf16); fills lse ([T][Hq] fp32) when given.
+    """
+    lib = load_library()
+    if workspace is None:
+        workspace = alloc_workspace(q.shape[1], k_pool, v_pool, batch, kv_split_tiles)
+    geo, out = _attn_args(q, k_pool, v_pool, batch, out, lse, workspace)
+    st = lib.gc_prefix_prefill_attention(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                         _opts(kv_split_tiles), q.data_ptr(), k_pool.data_ptr(),
+                                         v_pool.data_ptr(), float(scale), out.data_ptr(),
+                                         lse.data_ptr() if lse is not None else None,
+                                         workspace.data_ptr(), workspace.numel(),
+                                         _stream_handle(stream))
+    _check("gc_prefix_prefill_attention", st, lib)
+    return out

@@ -1,0 +1,328 @@
+// Host side of the C ABI declared in include/greencache.h: argument checks,
+// work-split policy, workspace layout and kernel launches. Every check runs
+// before the first HIP call, so invalid calls enqueue nothing.
+#include <cmath>
+#include <cstdint>
+#include <mutex>
+
+#include "gc_internal.h"
+#include "greencache.h"
+
+namespace {
+
+using gc::RequestCounts;
+
+struct Shape {
+    int64_t total_tokens = 0;
+    int group = 1;
+    int tq = 1;
+};
+
+struct Plan {
+    int chunk = 0;  // key tiles per chunk, 0 = no split
+    int64_t items = 0, combines = 0, partials = 0;
+    gc::WorkspaceLayout layout{};
+};
+
+gc_status check_common(const gc_geometry* geo, const gc_batch* b, Shape* sh) {
+    if (geo == nullptr || b == nullptr) return GC_ERR_NULL_ARG;
+    if (b->batch < 0) return GC_ERR_BAD_SHAPE;
+    if (geo->num_q_heads <= 0 || geo->num_kv_heads <= 0 || geo->head_dim <= 0 ||
+        geo->page_size <= 0 || geo->num_blocks < 0 || geo->max_blocks_per_seq < 0)
+        return GC_ERR_BAD_SHAPE;
+    if (geo->num_q_heads % geo->num_kv_heads != 0) return GC_ERR_BAD_SHAPE;
+    const int group = geo->num_q_heads / geo->num_kv_heads;
+    if (group > gc::kBlockM) return GC_ERR_UNSUPPORTED;
+    if (geo->head_dim != 64 && geo->head_dim != 128) return GC_ERR_UNSUPPORTED;
+    if (geo->page_size != gc::kPage) return GC_ERR_UNSUPPORTED;
+    sh->group = group;
+    sh->tq = gc::tokens_per_tile(group);
+    sh->total_tokens = 0;
+    if (b->batch == 0) return GC_OK;
+    if (b->prefix_lens_host == nullptr || b->new_lens_host == nullptr) return GC_ERR_NULL_ARG;
+    int64_t total = 0;
+    for (int r = 0; r < b->batch; ++r) {
+        const int64_t P = b->prefix_lens_host[r], n = b->new_lens_host[r];
+        if (P < 0 || n < 0) return GC_ERR_BAD_SHAPE;
+        if (P + n > (int64_t)INT32_MAX - gc::kBlockN) return GC_ERR_BAD_SHAPE;
+        total += n;
+    }
+    if (total > (int64_t)INT32_MAX) return GC_ERR_BAD_SHAPE;
+    for (int r = 0; r < b->batch; ++r) {
+        const int64_t P = b->prefix_lens_host[r], n = b->new_lens_host[r];
+        if (n > 0 && (P + n + gc::kPage - 1) / gc::kPage > geo->max_blocks_per_seq)
+            return GC_ERR_BLOCK_TABLE;
+    }
+    sh->total_tokens = total;
+    if (total > 0) {
+        if (geo->num_blocks <= 0) return GC_ERR_BAD_SHAPE;
+        if (b->prefix_lens_dev == nullptr || b->cu_new_lens_dev == nullptr ||
+            b->block_tables_dev == nullptr)
+            return GC_ERR_NULL_ARG;
+    }
+    return GC_OK;
+}
+
+gc_status check_options(const gc_plan_options* o) {
+    if (o == nullptr) return GC_OK;
+    for (int i = 0; i < 7; ++i)
+        if (o->reserved[i] != 0) return GC_ERR_BAD_SHAPE;
+    return GC_OK;
+}
+
+// Compute units of the current device (cached per device id).
+int device_cus() {
+    static std::mutex mu;
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+    if (dev < 64) {
+        std::lock_guard<std::mutex> g(mu);
+        if (cache[dev] > 0) return cache[dev];
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    if (dev < 64) {
+        std::lock_guard<std::mutex> g(mu);
+        cache[dev] = cus;
+    }
+    return cus;
+}
+
+// Split policy: keep whole query tiles when there are already several
+// workgroups per compute unit; otherwise cut the keys into chunks so that the
+// launch has about four workgroups per compute unit (two resident per CU, two
+// waves of them, longest first).
+int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
+                 const gc_plan_options* o) {
+    if (o != nullptr && o->kv_split_tiles != 0) return o->kv_split_tiles > 0 ? o->kv_split_tiles : 0;
+    int64_t units = 0, tiles = 0;
+    for (int r = 0; r < b->batch; ++r) {
+        const int P = b->prefix_lens_host[r], n = b->new_lens_host[r];
+        for (int q0 = 0; q0 < n; q0 += sh.tq) {
+            const int ntok = n - q0 < sh.tq ? n - q0 : sh.tq;
+            units += 1;
+            tiles += gc::key_tiles(P, q0, ntok);
+        }
+    }
+    units *= geo->num_kv_heads;
+    tiles *= geo->num_kv_heads;
+    const int64_t target = 4LL * device_cus();
+    if (units >= target || units == 0) return 0;
+    int64_t chunk = (tiles + target - 1) / target;
+    if (chunk < 8) chunk = 8;  // at least 512 keys per chunk
+    return chunk > INT32_MAX ? 0 : (int)chunk;
+}
+
+gc_status make_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
+                    const gc_plan_options* o, Plan* pl) {
+    pl->chunk = choose_chunk(geo, b, sh, o);
+    pl->items = pl->combines = pl->partials = 0;
+    for (int r = 0; r < b->batch; ++r) {
+        const RequestCounts c = gc::request_counts(b->prefix_lens_host[r], b->new_lens_host[r], sh.tq, pl->chunk);
+        pl->items += c.items;
+        pl->combines += c.combines;
+        pl->partials += c.partials;
+    }
+    if (pl->items > (int64_t)INT32_MAX / geo->num_kv_heads) return GC_ERR_BAD_SHAPE;
+    pl->layout = gc::workspace_layout(b->batch, pl->items, pl->combines, pl->partials,
+                                      geo->num_kv_heads, geo->head_dim);
+    return GC_OK;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+gc_status plan_checked(const gc_geometry* geo, const gc_batch* b, const gc_plan_options* o,
+                       Shape* sh, Plan* pl) {
+    gc_status st = check_common(geo, b, sh);
+    if (st != GC_OK) return st;
+    st = check_options(o);
+    if (st != GC_OK) return st;
+    if (sh->total_tokens == 0) return GC_OK;
+    return make_plan(geo, b, *sh, o, pl);
+}
+
+gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
+                       void* ws, hipStream_t stream) {
+    (void)geo;
+    gc::PlanArgs a{};
+    a.prefix_lens = b->prefix_lens_dev;
+    a.cu_new_lens = b->cu_new_lens_dev;
+    a.scratch = at<int32_t>(ws, pl.layout.scratch_off);
+    a.unsorted = reinterpret_cast<gc::WorkItem*>(
+        at<char>(ws, pl.layout.scratch_off) +
+        gc::align_up(sizeof(int32_t) * 3 * (size_t)(b->batch + 1), 256));
+    a.items = at<gc::WorkItem>(ws, pl.layout.items_off);
+    a.combines = at<gc::CombineItem>(ws, pl.layout.combine_off);
+    a.status = at<int32_t>(ws, pl.layout.status_off);
+    a.batch = b->batch;
+    a.tq = sh.tq;
+    a.chunk = pl.chunk;
+    a.expect_items = (int32_t)pl.items;
+    a.expect_combines = (int32_t)pl.combines;
+    a.expect_partials = (int32_t)pl.partials;
+    return gc::launch_plan(a, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+}
+
+gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
+                      const void* q, const void* k_pool, const void* v_pool, float scale,
+                      void* out, float* lse, void* ws, hipStream_t stream) {
+    gc::AttnArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k_pool = static_cast<const uint16_t*>(k_pool);
+    a.v_pool = static_cast<const uint16_t*>(v_pool);
+    a.out = static_cast<uint16_t*>(out);
+    a.lse = lse;
+    a.part_o = at<float>(ws, pl.layout.part_o_off);
+    a.part_lse = at<float>(ws, pl.layout.part_lse_off);
+    a.prefix_lens = b->prefix_lens_dev;
+    a.cu_new_lens = b->cu_new_lens_dev;
+    a.block_tables = b->block_tables_dev;
+    a.items = at<gc::WorkItem>(ws, pl.layout.items_off);
+    a.num_q_heads = geo->num_q_heads;
+    a.num_kv_heads = geo->num_kv_heads;
+    a.group = sh.group;
+    a.tq = sh.tq;
+    a.num_blocks = geo->num_blocks;
+    a.max_blocks = geo->max_blocks_per_seq;
+    a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
+    if (gc::launch_attention(a, geo->head_dim, pl.items, stream) != hipSuccess) return GC_ERR_HIP;
+    if (pl.combines > 0) {
+        gc::CombineArgs c{};
+        c.out = a.out;
+        c.lse = lse;
+        c.part_o = a.part_o;
+        c.part_lse = a.part_lse;
+        c.prefix_lens = b->prefix_lens_dev;
+        c.cu_new_lens = b->cu_new_lens_dev;
+        c.combines = at<gc::CombineItem>(ws, pl.layout.combine_off);
+        c.num_q_heads = geo->num_q_heads;
+        c.num_kv_heads = geo->num_kv_heads;
+        c.group = sh.group;
+        c.tq = sh.tq;
+        if (gc::launch_combine(c, geo->head_dim, pl.combines, stream) != hipSuccess) return GC_ERR_HIP;
+    }
+    return GC_OK;
+}
+
+gc_status check_run_args(const void* q, const void* k_pool, const void* v_pool, float scale,
+                         void* out) {
+    if (q == nullptr || k_pool == nullptr || v_pool == nullptr || out == nullptr)
+        return GC_ERR_NULL_ARG;
+    if (!std::isfinite(scale) || !(scale > 0.f)) return GC_ERR_BAD_SHAPE;
+    return GC_OK;
+}
+
+gc_status check_workspace(const Plan& pl, const void* ws, size_t bytes) {
+    if (ws == nullptr || bytes < pl.layout.total) return GC_ERR_WORKSPACE;
+    return GC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+__attribute__((visibility("default")))
+gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch, const void* k_new,
+                       const void* v_new, void* k_pool, void* v_pool, hipStream_t stream) {
+    Shape sh;
+    gc_status st = check_common(geo, batch, &sh);
+    if (st != GC_OK) return st;
+    if (sh.total_tokens == 0) return GC_OK;
+    if (k_new == nullptr || v_new == nullptr || k_pool == nullptr || v_pool == nullptr)
+        return GC_ERR_NULL_ARG;
+    gc::AppendArgs a{};
+    a.k_new = static_cast<const uint16_t*>(k_new);
+    a.v_new = static_cast<const uint16_t*>(v_new);
+    a.k_pool = static_cast<uint16_t*>(k_pool);
+    a.v_pool = static_cast<uint16_t*>(v_pool);
+    a.prefix_lens = batch->prefix_lens_dev;
+    a.cu_new_lens = batch->cu_new_lens_dev;
+    a.block_tables = batch->block_tables_dev;
+    a.batch = batch->batch;
+    a.total_tokens = (int32_t)sh.total_tokens;
+    a.num_kv_heads = geo->num_kv_heads;
+    a.num_blocks = geo->num_blocks;
+    a.max_blocks = geo->max_blocks_per_seq;
+    return gc::launch_append(a, geo->head_dim, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_workspace_size(const gc_geometry* geo, const gc_batch* batch,
+                                           const gc_plan_options* opts, size_t* bytes) {
+    if (bytes == nullptr) return GC_ERR_NULL_ARG;
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK) return st;
+    *bytes = sh.total_tokens == 0 ? 0 : pl.layout.total;
+    return GC_OK;
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_plan(const gc_geometry* geo, const gc_batch* batch,
+                                 const gc_plan_options* opts, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != GC_OK) return st;
+    return enqueue_plan(geo, batch, sh, pl, workspace, stream);
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_run(const gc_geometry* geo, const gc_batch* batch,
+                                const gc_plan_options* opts, const void* q, const void* k_pool,
+                                const void* v_pool, float scale, void* out, float* lse,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    st = check_run_args(q, k_pool, v_pool, scale, out);
+    if (st != GC_OK) return st;
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != GC_OK) return st;
+    return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream);
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* batch,
+                                      const gc_plan_options* opts, const void* q,
+                                      const void* k_pool, const void* v_pool, float scale,
+                                      void* out, float* lse, void* workspace,
+                                      size_t workspace_bytes, hipStream_t stream) {
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    st = check_run_args(q, k_pool, v_pool, scale, out);
+    if (st != GC_OK) return st;
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != GC_OK) return st;
+    st = enqueue_plan(geo, batch, sh, pl, workspace, stream);
+    if (st != GC_OK) return st;
+    return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream);
+}
+
+__attribute__((visibility("default")))
+const char* gc_status_string(gc_status s) {
+    switch (s) {
+        case GC_OK: return "GC_OK: success";
+        case GC_ERR_NULL_ARG: return "GC_ERR_NULL_ARG: a required pointer is NULL";
+        case GC_ERR_BAD_SHAPE: return "GC_ERR_BAD_SHAPE: invalid size, length or scale";
+        case GC_ERR_UNSUPPORTED: return "GC_ERR_UNSUPPORTED: head_dim must be 64 or 128, page_size 16, Hq/Hkv <= 128";
+        case GC_ERR_BLOCK_TABLE: return "GC_ERR_BLOCK_TABLE: block table too short for a request";
+        case GC_ERR_WORKSPACE: return "GC_ERR_WORKSPACE: workspace missing or too small";
+        case GC_ERR_HIP: return "GC_ERR_HIP: a HIP launch failed";
+    }
+    return "unknown gc_status";
+}
+
+}  // extern "C"

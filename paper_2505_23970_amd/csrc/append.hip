@@ -1,0 +1,91 @@
+// KV append for gfx950: copy the new tokens' K/V into their pool slots
+// (GreenCache §2.2, Fig. 1a step 1: the processed request's KV is saved so a
+// later request with the same context can reuse it).
+//
+// A workgroup takes 16 consecutive packed new tokens and walks the KV heads.
+// Keys are copied row by row (each 16-byte chunk read once, written once,
+// coalesced on both sides). Values go to transposed pages ([D][16]): the 16
+// tokens' rows are staged in LDS and written out column-wise, so the 16 lanes
+// that write one page row touch 32 consecutive bytes when the tokens share a
+// page. Slots whose block id is missing or outside the pool are skipped.
+#include "gc_internal.h"
+
+namespace gc {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendArgs a) {
+    constexpr int CPR = D / 8;        // 16-byte chunks per row
+    constexpr int kStride = D + 8;    // padded LDS row (elements)
+    __shared__ int32_t s_blk[kAppendTokens];
+    __shared__ int32_t s_off[kAppendTokens];
+    __shared__ __align__(16) uint16_t s_v[kAppendTokens * kStride];
+
+    const int tid = threadIdx.x;
+    const int tok0 = blockIdx.x * kAppendTokens;
+    const int ntok = min(kAppendTokens, a.total_tokens - tok0);
+
+    if (tid < kAppendTokens) {
+        int blk = -1, off = 0;
+        const int tok = tok0 + tid;
+        if (tid < ntok) {
+            // largest r with cu[r] <= tok; empty requests are skipped over
+            int lo = 0, hi = a.batch;
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (a.cu_new_lens[mid] <= tok) lo = mid;
+                else hi = mid;
+            }
+            const int pos = a.prefix_lens[lo] + (tok - a.cu_new_lens[lo]);
+            const int lp = pos / kPage;
+            off = pos % kPage;
+            if (lp < a.max_blocks) {
+                const int b = a.block_tables[(int64_t)lo * a.max_blocks + lp];
+                if (b >= 0 && b < a.num_blocks) blk = b;
+            }
+        }
+        s_blk[tid] = blk;
+        s_off[tid] = off;
+    }
+    __syncthreads();
+
+    for (int h = 0; h < a.num_kv_heads; ++h) {
+        for (int x = tid; x < kAppendTokens * CPR; x += kAppendThreads) {
+            const int tl = x / CPR, ch = x % CPR;
+            u32x4 v = u32x4{0u, 0u, 0u, 0u};
+            if (tl < ntok) {
+                const int64_t src = ((int64_t)(tok0 + tl) * a.num_kv_heads + h) * D + ch * 8;
+                const int blk = s_blk[tl];
+                if (blk >= 0) {
+                    const u32x4 k = *reinterpret_cast<const u32x4*>(a.k_new + src);
+                    *reinterpret_cast<u32x4*>(a.k_pool + (((int64_t)blk * a.num_kv_heads + h) * kPage + s_off[tl]) * D + ch * 8) = k;
+                }
+                v = *reinterpret_cast<const u32x4*>(a.v_new + src);
+            }
+            *reinterpret_cast<u32x4*>(&s_v[tl * kStride + ch * 8]) = v;
+        }
+        __syncthreads();
+        for (int x = tid; x < kAppendTokens * D; x += kAppendThreads) {
+            const int tl = x % kAppendTokens, d = x / kAppendTokens;
+            const int blk = s_blk[tl];
+            if (tl < ntok && blk >= 0)
+                a.v_pool[(((int64_t)blk * a.num_kv_heads + h) * D + d) * kPage + s_off[tl]] = s_v[tl * kStride + d];
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(a.total_tokens, kAppendTokens));
+    if (head_dim == 128)
+        append_kernel<128><<<grid, kAppendThreads, 0, s>>>(a);
+    else
+        append_kernel<64><<<grid, kAppendThreads, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace gc

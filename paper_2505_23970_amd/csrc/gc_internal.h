@@ -1,0 +1,163 @@
+// Internal declarations shared by the host library and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gc {
+
+// Attention tiling: a workgroup of 4 wavefronts owns 128 query rows
+// (query heads of one KV head stacked over consecutive new tokens) and walks
+// the request's keys in tiles of 64 (four 16-key pool pages).
+constexpr int kRowsPerWave = 32;
+constexpr int kWaves = 4;
+constexpr int kBlockM = kRowsPerWave * kWaves;  // 128
+constexpr int kBlockN = 64;
+constexpr int kPage = 16;
+constexpr int kAttnThreads = kWaves * 64;
+constexpr int kPlanThreads = 256;
+constexpr int kAppendTokens = 16;  // new tokens per append workgroup
+constexpr int kAppendThreads = 256;
+constexpr int kCostBuckets = 2048;  // counting-sort buckets of the work list (cost in tiles)
+
+// One attention work item: query tile [q0, q0 + tq) of request r against key
+// tiles [kt_begin, kt_end). part >= 0 marks a split item whose normalised
+// partial output goes to partial slot `part`; -1 writes the output directly.
+struct WorkItem {
+    int32_t r, q0, kt_begin, kt_end, part, pad0, pad1, pad2;
+};
+
+// One query tile whose keys were split: partial slots [part_base, part_base + ns).
+struct CombineItem {
+    int32_t r, q0, part_base, ns;
+};
+
+// ---------------------------------------------------------------- plan math
+// Used by the host (grid sizes, workspace) and the planner kernel (the list
+// itself); both must agree exactly.
+
+__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// new tokens per query tile for a GQA group of g query heads per KV head
+__host__ __device__ inline int tokens_per_tile(int group) { return kBlockM / group; }
+
+__host__ __device__ inline int key_tiles(int prefix, int q0, int ntok) {
+    return ceil_div(prefix + q0 + ntok, kBlockN);
+}
+
+// number of key chunks of a query tile with kt key tiles; chunk <= 0 means never split
+__host__ __device__ inline int num_splits(int kt, int chunk) {
+    return (chunk <= 0 || kt <= chunk) ? 1 : ceil_div(kt, chunk);
+}
+
+// first key tile of chunk s out of ns (balanced; every chunk non-empty when ns <= kt)
+__host__ __device__ inline int split_begin(int s, int kt, int ns) {
+    return (int)(((int64_t)s * kt) / ns);
+}
+
+struct RequestCounts {
+    int items;     // work items of this request (per KV head)
+    int combines;  // query tiles that were split
+    int partials;  // partial slots (per KV head)
+};
+
+__host__ __device__ inline RequestCounts request_counts(int prefix, int n, int tq, int chunk) {
+    RequestCounts c{0, 0, 0};
+    for (int q0 = 0; q0 < n; q0 += tq) {
+        int ntok = n - q0 < tq ? n - q0 : tq;
+        int ns = num_splits(key_tiles(prefix, q0, ntok), chunk);
+        c.items += ns;
+        if (ns > 1) {
+            c.combines += 1;
+            c.partials += ns;
+        }
+    }
+    return c;
+}
+
+// ---------------------------------------------------------------- workspace
+struct WorkspaceLayout {
+    size_t items_off, combine_off, scratch_off, part_lse_off, part_o_off, status_off, total;
+};
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+inline WorkspaceLayout workspace_layout(int batch, int64_t items, int64_t combines,
+                                        int64_t partials, int num_kv_heads, int head_dim) {
+    WorkspaceLayout w{};
+    size_t off = 0;
+    w.status_off = off;
+    off = align_up(off + 256, 256);
+    w.items_off = off;
+    off = align_up(off + sizeof(WorkItem) * (size_t)(items > 0 ? items : 1), 256);
+    w.combine_off = off;
+    off = align_up(off + sizeof(CombineItem) * (size_t)(combines > 0 ? combines : 1), 256);
+    w.scratch_off = off;  // 3 int32 per request + 1, then the unsorted work list
+    off = align_up(off + sizeof(int32_t) * 3 * (size_t)(batch + 1), 256);
+    off = align_up(off + sizeof(WorkItem) * (size_t)(items > 0 ? items : 1), 256);
+    w.part_lse_off = off;
+    off = align_up(off + sizeof(float) * (size_t)partials * num_kv_heads * kBlockM, 256);
+    w.part_o_off = off;
+    off = align_up(off + sizeof(float) * (size_t)partials * num_kv_heads * kBlockM * head_dim, 256);
+    w.total = off;
+    return w;
+}
+
+// ---------------------------------------------------------------- kernel launch arguments
+struct AppendArgs {
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    uint16_t* k_pool;
+    uint16_t* v_pool;
+    const int32_t* prefix_lens;
+    const int32_t* cu_new_lens;
+    const int32_t* block_tables;
+    int32_t batch, total_tokens, num_kv_heads, num_blocks, max_blocks;
+};
+
+struct PlanArgs {
+    const int32_t* prefix_lens;
+    const int32_t* cu_new_lens;
+    int32_t* scratch;         // 3 * (batch + 1) int32
+    WorkItem* unsorted;       // [items]
+    WorkItem* items;          // [items], sorted by cost, heaviest first
+    CombineItem* combines;    // [combines]
+    int32_t* status;          // status[0] = 0 when the device counts matched the host's
+    int32_t batch, tq, chunk;
+    int32_t expect_items, expect_combines, expect_partials;
+};
+
+struct AttnArgs {
+    const uint16_t* q;
+    const uint16_t* k_pool;
+    const uint16_t* v_pool;
+    uint16_t* out;
+    float* lse;          // may be null
+    float* part_o;       // [partials][Hkv][128][D]
+    float* part_lse;     // [partials][Hkv][128]
+    const int32_t* prefix_lens;
+    const int32_t* cu_new_lens;
+    const int32_t* block_tables;
+    const WorkItem* items;
+    int32_t num_q_heads, num_kv_heads, group, tq;
+    int32_t num_blocks, max_blocks;
+    float scale_log2;    // softmax scale * log2(e)
+};
+
+struct CombineArgs {
+    uint16_t* out;
+    float* lse;
+    const float* part_o;
+    const float* part_lse;
+    const int32_t* prefix_lens;
+    const int32_t* cu_new_lens;
+    const CombineItem* combines;
+    int32_t num_q_heads, num_kv_heads, group, tq;
+};
+
+hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
+hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s);
+
+}  // namespace gc

@@ -1,0 +1,250 @@
+"""HIP path vs. the fp64 oracle, element by element, through the C ABI (GPU)."""
+import sys
+
+import numpy as np
+import pytest
+
+import gpu_helpers as H
+from paper_2505_23970_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu_ready():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2505_23970_amd as gc
+    gc.load_library()  # raises if the HIP library is missing: there is no other path
+
+
+def check_pool(run: H.DeviceRun, kp_ref, vp_ref):
+    kp = H.from_dev_bits(run.k_pool)
+    vp = H.from_dev_bits(run.v_pool)
+    assert np.array_equal(kp, kp_ref), f"k_pool differs at {np.argwhere(kp != kp_ref)[:5]}"
+    assert np.array_equal(vp, vp_ref), f"v_pool differs at {np.argwhere(vp != vp_ref)[:5]}"
+
+
+def full_check(w, kv_split_tiles=None, rows=None, contract=True):
+    say(f"case {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
+        f"T={w.total_new} split={kv_split_tiles}")
+    kp_ref, vp_ref = H.oracle_pools(w)
+    run = H.DeviceRun(w)
+    run.append()
+    check_pool(run, kp_ref, vp_ref)
+    out, lse = run.attention(kv_split_tiles=kv_split_tiles)
+    ref_out, ref_lse = H.oracle_rows(w, kp_ref, vp_ref, rows=rows)
+    return H.compare_attention(w, out, lse, ref_out, ref_lse, rows=rows, contract=contract), run, out
+
+
+# ----------------------------------------------------------------- the five workloads
+
+@pytest.mark.parametrize("k", [1, 2])
+def test_config_all_rows(k):
+    w = W.make_config(k)
+    info, _, _ = full_check(w)
+    say(f"config {k}: {info}")
+
+
+@pytest.mark.parametrize("k", [3, 4, 5])
+def test_config_sampled_rows(k):
+    w = W.make_config(k)
+    rows = H.sample_rows(w, seed=k)
+    info, _, _ = full_check(w, rows=rows)
+    say(f"config {k}: {len(rows)} rows {info}")
+
+
+def test_short_suffix_variant_sampled():
+    w = W.short_suffix_variant()
+    info, _, _ = full_check(w, rows=H.sample_rows(w, seed=40))
+    say(f"long reuse, 16 new tokens: {info}")
+
+
+# ----------------------------------------------------------------- supplementary suites
+
+SUITE_SHAPE = dict(prefix_lens=[300, 1000, 33, 0], new_lens=[77, 20, 130, 45],
+                   num_q_heads=16, num_kv_heads=2, head_dim=128)
+
+
+@pytest.mark.parametrize("values", ["unit", "peaked"])
+@pytest.mark.parametrize("split", [None, 2])
+def test_value_scales(values, split):
+    w = W.build(seed=100, values=values, name=f"suite_{values}", **SUITE_SHAPE)
+    full_check(w, kv_split_tiles=split)
+
+
+@pytest.mark.parametrize("split", [None, 1])
+def test_needle_in_prefix_and_in_new_tokens(split):
+    w = W.build(seed=101, name="needles", **SUITE_SHAPE)
+    # request 0: needle in a random prefix page; request 2: needle among the new
+    # tokens at position P + 50 (rows before it must not see it)
+    W.plant_needles(w, [(0, 137), (1, 999), (2, 33 + 50)])
+    info, run, out = full_check(w, kv_split_tiles=split)
+    got = H.from_dev_f32(out)
+    vn = W.bf16_bits_to_f32(w.v_new).astype(np.float64)
+    vpre = W.bf16_bits_to_f32(w.v_prefix).astype(np.float64)
+    cu, cup = w.cu_new_lens, w.cu_prefix_lens
+    g = w.num_q_heads // w.num_kv_heads
+    # request 0 rows all return the needle's value (weight >= 1 - 3e-6)
+    for t in range(int(cu[0]), int(cu[1])):
+        for h in range(w.num_q_heads):
+            np.testing.assert_allclose(got[t, h], vpre[cup[0] + 137, h // g], atol=2e-2)
+    # request 2: rows i >= 50 see V[needle], rows i < 50 do not
+    needle_v = vn[cu[2] + 50]
+    for i in range(int(w.new_lens[2])):
+        t = int(cu[2]) + i
+        for h in range(0, w.num_q_heads, 5):
+            close = np.allclose(got[t, h], needle_v[h // g], atol=2e-2)
+            assert close == (i >= 50), (i, h)
+
+
+@pytest.mark.parametrize("split", [None, 1])
+def test_values_one_normalises(split):
+    """V = 1: the output is the sum of the weights. The probabilities enter the PV
+    product rounded to bf16 (relative error <= 2^-8 each) while the normaliser sums
+    them unrounded, so the result is 1 within 2^-8 and then rounds to 1.0 or to
+    the bf16 value just below it; nearly every row lands exactly on 1.0."""
+    w = W.set_values_one(W.build(seed=102, values="unit", name="v_one", **SUITE_SHAPE))
+    _, _, out = full_check(w, kv_split_tiles=split)
+    got = H.from_dev_f32(out)
+    assert np.all(np.abs(got - 1.0) <= 2.0 ** -8)
+    assert np.mean(got == 1.0) >= 0.99
+
+
+@pytest.mark.parametrize("split", [None, 1])
+def test_position_code_window(split):
+    w = W.set_position_code(W.build([0, 17, 64, 200, 15], [100, 60, 1, 56, 241], 8, 2, 64,
+                                    seed=103, name="poscode"))
+    _, _, out = full_check(w, kv_split_tiles=split)
+    got = H.from_dev_f32(out)[:, :, 0]
+    cu = w.cu_new_lens
+    for r in range(w.batch):
+        for i in range(int(w.new_lens[r])):
+            expect = (int(w.prefix_lens[r]) + i) / 2.0
+            assert np.all(got[cu[r] + i] == expect), (r, i, got[cu[r] + i], expect)
+
+
+# ----------------------------------------------------------------- edge cases
+
+EDGES = [
+    ("miss_only", [0], [1], 8, 1, 128),
+    ("single_token_decode_shape", [777], [1], 32, 8, 128),
+    ("page_boundaries", [16, 1, 15, 32, 0], [16, 15, 17, 1, 16], 8, 2, 128),
+    ("mha", [100, 50], [30, 70], 4, 4, 64),
+    ("group3_odd_tile", [40, 130], [100, 9], 6, 2, 128),
+    ("group16", [500], [40], 32, 2, 128),
+    ("group128_one_token_tiles", [300], [5], 128, 1, 64),
+    ("zero_length_requests", [10, 5, 0, 70], [0, 20, 0, 33], 8, 8, 128),
+    ("batch32_short", list(range(0, 320, 10)), [3] * 16 + [65] * 16, 8, 1, 128),
+    ("tile_multiple_suffix", [64], [128], 8, 1, 128),
+]
+
+
+@pytest.mark.parametrize("name,P,n,Hq,Hkv,D", EDGES, ids=[e[0] for e in EDGES])
+def test_edge_cases(name, P, n, Hq, Hkv, D):
+    w = W.build(P, n, Hq, Hkv, D, seed=200 + EDGES.index((name, P, n, Hq, Hkv, D)),
+                values="unit", name=name)
+    full_check(w)
+    full_check(w, kv_split_tiles=1)
+
+
+def test_longest_prefix_sampled():
+    w = W.build([200_000], [40], 8, 1, 128, seed=250, name="longest")
+    rows = np.array([0, 7, 8 * 20 + 3, 8 * 39, 8 * 39 + 7], np.int64)
+    full_check(w, rows=rows)
+
+
+# ----------------------------------------------------------------- determinism and invariants
+
+def test_split_is_deterministic_and_close_to_unsplit():
+    w = W.build([3000, 100], [50, 200], 16, 2, 128, seed=300, values="unit")
+    run = H.DeviceRun(w)
+    run.append()
+    a, _ = run.attention(kv_split_tiles=3)
+    b, _ = run.attention(kv_split_tiles=3)
+    c, _ = run.attention(kv_split_tiles=-1)
+    assert np.array_equal(H.from_dev_bits(a), H.from_dev_bits(b))
+    d1 = H.from_dev_f32(a) - H.from_dev_f32(c)
+    assert np.abs(d1).max() <= 2 ** -6
+
+
+def test_block_relabelling_is_bitwise_invisible():
+    w = W.build([123, 45], [40, 90], 8, 2, 128, seed=301, values="unit")
+    run1 = H.DeviceRun(w)
+    run1.append()
+    o1, l1 = run1.attention()
+    perm = np.random.default_rng(3).permutation(w.num_blocks)
+    w2 = W.Workload(**{f.name: getattr(w, f.name) for f in W.dataclasses.fields(W.Workload)})
+    w2.block_tables = perm[w.block_tables].astype(np.int32)
+    w2.finish()
+    run2 = H.DeviceRun(w2)
+    run2.append()
+    o2, l2 = run2.attention()
+    assert np.array_equal(H.from_dev_bits(o1), H.from_dev_bits(o2))
+    assert np.array_equal(H.from_dev_f32(l1), H.from_dev_f32(l2))
+
+
+def test_plan_once_run_twice():
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build([500, 20], [70, 33], 16, 2, 128, seed=302)
+    run = H.DeviceRun(w)
+    run.append()
+    ws = gc.alloc_workspace(w.num_q_heads, run.k_pool, run.v_pool, run.batch, kv_split_tiles=2)
+    gc.plan(w.num_q_heads, run.k_pool, run.v_pool, run.batch, ws, kv_split_tiles=2)
+    o1 = gc.run(run.q, run.k_pool, run.v_pool, run.batch, w.scale, ws, kv_split_tiles=2)
+    o2 = gc.run(run.q, run.k_pool, run.v_pool, run.batch, w.scale, ws, kv_split_tiles=2)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.from_dev_bits(o1), H.from_dev_bits(o2))
+    kp, vp = H.oracle_pools(w)
+    ref, _ = H.oracle_rows(w, kp, vp)
+    H.compare_attention(w, o1, None, ref, None)
+
+
+def test_two_turns_equal_one_call():
+    """Multi-turn reuse: turn 1 appends n1 tokens and attends; turn 2 treats them as
+    cached prefix. The rows match a single call over n1 + n2 new tokens."""
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build([200], [90], 8, 2, 128, seed=303, values="unit")
+    one = H.DeviceRun(w)
+    one.append()
+    full, _ = one.attention()
+    n1 = 37
+    dev = H.DeviceRun(w)
+    b1 = gc.PagedBatch(w.prefix_lens, [n1], w.block_tables)
+    gc.kv_append(dev.k_new[:n1].contiguous(), dev.v_new[:n1].contiguous(), dev.k_pool, dev.v_pool, b1)
+    o1 = gc.prefix_prefill_attention(dev.q[:n1].contiguous(), dev.k_pool, dev.v_pool, b1, w.scale)
+    b2 = gc.PagedBatch(w.prefix_lens + n1, [90 - n1], w.block_tables)
+    gc.kv_append(dev.k_new[n1:].contiguous(), dev.v_new[n1:].contiguous(), dev.k_pool, dev.v_pool, b2)
+    o2 = gc.prefix_prefill_attention(dev.q[n1:].contiguous(), dev.k_pool, dev.v_pool, b2, w.scale)
+    torch.cuda.synchronize()
+    got = np.concatenate([H.from_dev_f32(o1), H.from_dev_f32(o2)])
+    assert np.abs(got - H.from_dev_f32(full)).max() <= 2 ** -7
+
+
+def test_append_leaves_other_slots_alone_with_bad_block_ids():
+    """Table entries outside the pool are skipped by the append kernel; every
+    other slot is written exactly as the oracle writes it."""
+    w = W.build([20, 3], [30, 40], 8, 2, 128, seed=304)
+    bad = w.block_tables.copy()
+    bad[1, 2] = w.num_blocks + 5   # page 2 of request 1 (positions 32..47)
+    run = H.DeviceRun(w)
+    run.batch = __import__("paper_2505_23970_amd").PagedBatch(w.prefix_lens, w.new_lens, bad)
+    run.append()
+    import torch
+    torch.cuda.synchronize()
+    kp_ref, vp_ref = H.oracle_pools(w)
+    kp = H.from_dev_bits(run.k_pool)
+    vp = H.from_dev_bits(run.v_pool)
+    skipped = int(w.block_tables[1, 2])
+    keep = np.ones(w.num_blocks, bool)
+    keep[skipped] = False
+    assert np.array_equal(kp[keep], kp_ref[keep]) and np.array_equal(vp[keep], vp_ref[keep])
+    assert np.array_equal(kp[skipped], w.k_pool[skipped])   # untouched
