@@ -1,0 +1,194 @@
+#!/usr/bin/env python3
+"""Benchmark of the prefix-cached prefill path on one MI355X.
+
+One step = the whole hot path over one batch already resident in HBM:
+KV append of the new tokens (gc_kv_append), work-list planning
+(gc_prefix_prefill_plan) and attention (gc_prefix_prefill_run). The default
+workload is the Llama-3-8B attention shape (32 query / 8 KV heads, head_dim
+128, 8 ragged requests with cached prefixes of 1024-4096 tokens and 64-512
+new tokens, page 16, random block permutation), drawn from a fixed seed.
+
+Prints one JSON line: throughput (attention TFLOP/s over the step, and new
+tokens/s), the dominant kernel's roofline figures measured with HIP events on
+the launch stream, and the fp64 CPU oracle timed on a bounded sample of the
+same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "prefix-cached prefill attn TFLOP/s + new tokens/s; % of bf16 MFMA/HBM roof"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+WORKLOADS = {
+    "tiny": lambda: _cfg(1),
+    "llama3_8b": lambda: _cfg(2),
+    "llama3_70b_chat": lambda: _cfg(3),
+    "long_reuse_70b": lambda: _cfg(4),
+    "mixed_hit_miss_70b": lambda: _cfg(5),
+    "long_reuse_70b_n16": lambda: _short(),
+}
+
+
+def _cfg(k):
+    from paper_2505_23970_amd import workloads as W
+    return W.make_config(k)
+
+
+def _short():
+    from paper_2505_23970_amd import workloads as W
+    return W.short_suffix_variant()
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3_8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--kv-split-tiles", type=int, default=None,
+                    help="override the automatic split policy (0 auto, <0 never, >0 tiles)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target duration of the CPU-oracle sample (0 disables it)")
+    return ap.parse_args()
+
+
+def cpu_oracle_baseline(w, target_s):
+    """Time the fp64 oracle on a bounded sample of the workload's output rows."""
+    import oracle
+    kp, vp = oracle.kv_append(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                              w.k_new, w.v_new, w.k_pool, w.v_pool)
+    T, Hq, D = w.q.shape
+    cu = w.cu_new_lens
+    req = np.repeat(np.arange(w.batch), w.new_lens)
+    pos = w.prefix_lens[req] + (np.arange(T) - cu[req])        # logical position per token
+    keys_per_token = pos.astype(np.float64) + 1.0
+    rng = np.random.default_rng(12345)
+    order = rng.permutation(T * Hq)
+    threads = oracle.max_threads()
+
+    def timed(rows):
+        t0 = time.perf_counter()
+        oracle.attention(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q, kp, vp,
+                         w.scale, rows=rows)
+        return time.perf_counter() - t0
+
+    # calibrate on a small slice, then size the sample to about target_s seconds
+    n_cal = min(len(order), max(64, threads * 8))
+    cal = np.sort(order[:n_cal])
+    t_cal = max(timed(cal), 1e-6)
+    n_rows = int(min(len(order), max(n_cal, n_cal * target_s / t_cal)))
+    rows = np.sort(order[:n_rows])
+    t = timed(rows)
+    flops = float(np.sum(4.0 * D * keys_per_token[rows // Hq]))
+    sample = (f"{n_rows} of {T * Hq} output rows (token, query head) drawn uniformly at random; "
+              f"fp64 oracle, append excluded")
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": sample, "seconds": t,
+            "new_tokens_per_s_equiv": (n_rows / Hq) / t}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(this path has no multi-GPU mode)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2505_23970_amd as gc
+
+    gc.load_library()
+    w = WORKLOADS[args.workload]()
+    F = w.flops()
+    T, Hq, D = w.q.shape
+    dev = torch.device("cuda")
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    batch = gc.PagedBatch(w.prefix_lens, w.new_lens, w.block_tables, device=dev)
+    q, k_new, v_new = up(w.q), up(w.k_new), up(w.v_new)
+    k_pool, v_pool = up(w.k_pool), up(w.v_pool)
+    out = torch.empty_like(q)
+    ws = gc.alloc_workspace(Hq, k_pool, v_pool, batch, args.kv_split_tiles)
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        gc.kv_append(k_new, v_new, k_pool, v_pool, batch)
+        if ev is not None:
+            ev[1].record()
+        gc.plan(Hq, k_pool, v_pool, batch, ws, args.kv_split_tiles)
+        if ev is not None:
+            ev[2].record()
+        gc.run(q, k_pool, v_pool, batch, w.scale, ws, out=out, kv_split_tiles=args.kv_split_tiles)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps, host clock around the stream
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    app = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    pln = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    att = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    t_att = float(np.mean(att)) * 1e-3
+
+    achieved = F / t_att / 1e12
+    rec = {
+        "metric": METRIC,
+        "value": F / (ms_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, **{k: v for k, v in w.describe().items() if k != "workload"},
+                   "kv_split_tiles": args.kv_split_tiles},
+        "new_tokens_per_s": T / (ms_step * 1e-3),
+        "attention_tflops": achieved,
+        "kernel_ms": {"append": float(np.mean(app)), "plan": float(np.mean(pln)),
+                      "attention": float(np.mean(att)),
+                      "attention_p10": float(np.percentile(att, 10)),
+                      "attention_p90": float(np.percentile(att, 90))},
+        "algorithmic": {"flops": F, "attn_bytes": w.attn_bytes(), "append_bytes": w.append_bytes()},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "attention_kernel<128> (+ split merge when the plan splits)",
+                     "hbm_gbs_algorithmic": w.attn_bytes() / t_att / 1e9},
+    }
+    if args.cpu_seconds > 0:
+        rec["cpu_baseline"] = cpu_oracle_baseline(w, args.cpu_seconds)
+    else:
+        rec["cpu_baseline"] = None
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

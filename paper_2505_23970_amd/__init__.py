@@ -130,8 +130,8 @@ class PagedBatch:
         cu = np.zeros(self.prefix_lens.shape[0] + 1, np.int32)
         np.cumsum(self.new_lens, out=cu[1:])
         self.cu_new_lens = cu
-        self.device = torch.device(device)
-        self.prefix_lens_dev = torch.from_numpy(self.prefix_lens.copy()).to(self.device)
+        self.prefix_lens_dev = torch.from_numpy(self.prefix_lens.copy()).to(device)
+        self.device = self.prefix_lens_dev.device  # concrete, e.g. cuda:0
         self.cu_new_lens_dev = torch.from_numpy(cu.copy()).to(self.device)
         self.block_tables_dev = torch.from_numpy(bt.copy()).to(self.device)
         self._desc = BatchDesc(

@@ -31,7 +31,9 @@ def check_pool(run: H.DeviceRun, kp_ref, vp_ref):
     assert np.array_equal(vp, vp_ref), f"v_pool differs at {np.argwhere(vp != vp_ref)[:5]}"
 
 
-def full_check(w, kv_split_tiles=None, rows=None, contract=True):
+def full_check(w, kv_split_tiles=None, rows=None, contract=False):
+    """Append + attention on the GPU vs. the oracle. `contract` adds the fixed
+    max/mean absolute bounds, which are stated for the configs' value scale."""
     say(f"case {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
         f"T={w.total_new} split={kv_split_tiles}")
     kp_ref, vp_ref = H.oracle_pools(w)
@@ -48,7 +50,7 @@ def full_check(w, kv_split_tiles=None, rows=None, contract=True):
 @pytest.mark.parametrize("k", [1, 2])
 def test_config_all_rows(k):
     w = W.make_config(k)
-    info, _, _ = full_check(w)
+    info, _, _ = full_check(w, contract=True)
     say(f"config {k}: {info}")
 
 
@@ -56,13 +58,13 @@ def test_config_all_rows(k):
 def test_config_sampled_rows(k):
     w = W.make_config(k)
     rows = H.sample_rows(w, seed=k)
-    info, _, _ = full_check(w, rows=rows)
+    info, _, _ = full_check(w, rows=rows, contract=True)
     say(f"config {k}: {len(rows)} rows {info}")
 
 
 def test_short_suffix_variant_sampled():
     w = W.short_suffix_variant()
-    info, _, _ = full_check(w, rows=H.sample_rows(w, seed=40))
+    info, _, _ = full_check(w, rows=H.sample_rows(w, seed=40), contract=True)
     say(f"long reuse, 16 new tokens: {info}")
 
 
