@@ -61,7 +61,21 @@ def parse():
                     help="override the automatic split policy (0 auto, <0 never, >0 tiles)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU-oracle sample (0 disables it)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="instead of the benchmark, run 5 plain device-to-device copies of this "
+                         "many MiB (reference point that scales hardware byte counters)")
     return ap.parse_args()
+
+
+def copy_reference(mib):
+    import torch
+    n = mib * (1 << 20)
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
 
 
 def cpu_oracle_baseline(w, target_s):
@@ -105,6 +119,9 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(this path has no multi-GPU mode)", file=sys.stderr)
         sys.exit(2)
+    if args.copy_mib > 0:
+        copy_reference(args.copy_mib)
+        return
     import torch
     import paper_2505_23970_amd as gc
 

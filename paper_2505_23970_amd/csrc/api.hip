@@ -90,10 +90,9 @@ int device_cus() {
     return cus;
 }
 
-// Split policy: keep whole query tiles when there are already several
-// workgroups per compute unit; otherwise cut the keys into chunks so that the
-// launch has about four workgroups per compute unit (two resident per CU, two
-// waves of them, longest first).
+// Split policy: keep whole query tiles when there are at least as many
+// workgroups as resident slots (two per compute unit); otherwise cut the keys
+// into chunks so that the launch fills those slots.
 int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
                  const gc_plan_options* o) {
     if (o != nullptr && o->kv_split_tiles != 0) return o->kv_split_tiles > 0 ? o->kv_split_tiles : 0;
@@ -108,7 +107,7 @@ int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
     }
     units *= geo->num_kv_heads;
     tiles *= geo->num_kv_heads;
-    const int64_t target = 4LL * device_cus();
+    const int64_t target = 2LL * device_cus();
     if (units >= target || units == 0) return 0;
     int64_t chunk = (tiles + target - 1) / target;
     if (chunk < 8) chunk = 8;  // at least 512 keys per chunk
@@ -204,6 +203,8 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
         c.num_kv_heads = geo->num_kv_heads;
         c.group = sh.group;
         c.tq = sh.tq;
+        c.batch = b->batch;
+        c.num_partials = (int32_t)pl.partials;
         if (gc::launch_combine(c, geo->head_dim, pl.combines, stream) != hipSuccess) return GC_ERR_HIP;
     }
     return GC_OK;

@@ -32,6 +32,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
 
@@ -41,7 +42,6 @@ __device__ __forceinline__ int swz_k(int chunk, int row) {
     if constexpr (D == 128) return chunk ^ (row & 15);  // 256-byte rows
     else return chunk ^ ((row >> 1) & 7);                // 128-byte rows
 }
-__device__ __forceinline__ int swz_v(int chunk, int drow) { return chunk ^ ((drow >> 1) & 7); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     __bf16 a = (__bf16)lo;
@@ -49,19 +49,32 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
+// Uniform loads through the constant address space become scalar loads.
+typedef const __attribute__((address_space(4))) int32_t* scalar_i32p;
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
 template <int D>
 __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnArgs a) {
-    constexpr int DK = D / 16;               // k-steps of QK^T
-    constexpr int DB = D / 32;               // 32-row blocks of O^T
-    constexpr int NCH = D / 32;              // 16-byte chunks per thread per tile per tensor
-    constexpr int kPagesPerPass = kAttnThreads / (2 * D);
+    constexpr int DK = D / 16;                      // k-steps of QK^T
+    constexpr int DB = D / 32;                      // 32-row blocks of O^T
+    constexpr int kPageBytes = kPage * D * 2;       // one (block, KV head) page of K or V
+    constexpr int kTileBytes = kBlockN * D * 2;     // four pages
+    constexpr int kKbPerPage = kPageBytes / 1024;   // 1 KiB pieces per page
+    constexpr int NI = kTileBytes / (kWaves * 1024);  // direct loads per wave per tensor per tile
+    constexpr int kTileLog2Thresh = 8;              // rescale only when the max grows by > 2^8
 
-    __shared__ __align__(16) uint16_t k_lds[2][kBlockN * D];
-    __shared__ __align__(16) uint16_t v_lds[2][D * kBlockN];
+    // K tile: [64 keys][D], row-major, 16-byte chunks XOR-swizzled by row.
+    // V tile: 4 pages of [D][16 keys], the two 16-byte halves of a row swapped on odd 8-row groups.
+    // Two separate buffers of each (distinct objects, so the compiler can tell that
+    // reads of one do not wait for the asynchronous loads into the other).
+    __shared__ __align__(16) unsigned char k_lds0[kTileBytes];
+    __shared__ __align__(16) unsigned char v_lds0[kTileBytes];
+    __shared__ __align__(16) unsigned char k_lds1[kTileBytes];
+    __shared__ __align__(16) unsigned char v_lds1[kTileBytes];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hh = lane >> 5;
     const int lr = lane & 31;
     const int kvh = (int)(blockIdx.x % (unsigned)a.num_kv_heads);
@@ -94,73 +107,66 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
         for (int k = 0; k < DK; ++k) qf[k] = __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
     }
 
-    // staging assignment: page (e * kPagesPerPass + pip) of the tile
-    const int pip = tid / (2 * D);
-    const int idx = tid % (2 * D);
-    const int k_slot = idx / (D / 8), k_chunk = idx % (D / 8);
-    const int v_row = idx >> 1, v_half = idx & 1;
-    u32x4 kreg[NCH], vreg[NCH];
+    // Direct global->LDS loads: instruction e of a wave moves 1 KiB piece 4e + wave of
+    // a tile tensor, i.e. piece `sub` of page `page_of(e)`; lane i lands at byte 16 i.
+    const int sub = wave % kKbPerPage;
+    auto page_of = [&](int e) -> int { return kKbPerPage == 4 ? e : (4 * e + wave) / kKbPerPage; };
+    const int k_row = sub * (1024 / (2 * D)) + lane / (D / 8);         // key slot in the page
+    const uint32_t k_src = k_row * (2 * D) + swz_k<D>(lane % (D / 8), k_row) * 16;
+    const int v_d = sub * 32 + (lane >> 1);                            // value row (d) in the page
+    const int v_half = (lane & 1) ^ ((v_d >> 3) & 1);                  // logical half held by the lane
+    const uint32_t v_src = v_d * 32 + v_half * 16;
+    const scalar_i32p table = (scalar_i32p)(a.block_tables + (int64_t)r * a.max_blocks);
+    const int64_t head_off = (int64_t)kvh * kPageBytes;
+    const int64_t block_stride = (int64_t)a.num_kv_heads * kPageBytes;
 
-    auto load_tile = [&](int kt) {
+    // raw table entries of tile kt (indices clamped into the row; checked at use)
+    auto fetch_ids = [&](int kt, int (&ids)[4]) {
 #pragma unroll
-        for (int e = 0; e < NCH; ++e) {
-            const int p = e * kPagesPerPass + pip;
-            const int lp = kt * (kBlockN / kPage) + p;
-            int blk = -1;
-            if (lp * kPage < L && lp < a.max_blocks) {
-                blk = a.block_tables[(int64_t)r * a.max_blocks + lp];
-                if (blk >= a.num_blocks) blk = -1;
-            }
-            if (blk >= 0) {
-                const int64_t base = ((int64_t)blk * a.num_kv_heads + kvh) * (kPage * D);
-                kreg[e] = *reinterpret_cast<const u32x4*>(a.k_pool + base + k_slot * D + k_chunk * 8);
-                u32x4 v = *reinterpret_cast<const u32x4*>(a.v_pool + base + v_row * kPage + v_half * 8);
-                const int j0 = lp * kPage + v_half * 8;
-                if (j0 + 8 > L) {  // value slots at or past the sequence end become 0
+        for (int p = 0; p < 4; ++p) ids[p] = table[min(kt * 4 + p, a.max_blocks - 1)];
+    };
+    auto issue_tile = [&](unsigned char* kdst, unsigned char* vdst, int kt, const int (&ids)[4]) {
 #pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        uint32_t keep = (j0 + 2 * w < L ? 0x0000FFFFu : 0u) |
-                                        (j0 + 2 * w + 1 < L ? 0xFFFF0000u : 0u);
-                        v[w] &= keep;
-                    }
-                }
-                vreg[e] = v;
-            } else {
-                kreg[e] = u32x4{0u, 0u, 0u, 0u};
-                vreg[e] = u32x4{0u, 0u, 0u, 0u};
+        for (int e = 0; e < NI; ++e) {
+            const int pg = page_of(e);
+            const int lp = kt * 4 + pg;
+            const int blk = ids[pg];
+            if (lp < a.max_blocks && lp * kPage < L && blk >= 0 && blk < a.num_blocks) {
+                const int64_t base = (int64_t)blk * block_stride + head_off;
+                const unsigned char* kg = reinterpret_cast<const unsigned char*>(a.k_pool) + base;
+                const unsigned char* vg = reinterpret_cast<const unsigned char*>(a.v_pool) + base;
+                __builtin_amdgcn_global_load_lds(kg + k_src, (lds_ptr)(kdst + pg * kPageBytes + sub * 1024), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds(vg + v_src, (lds_ptr)(vdst + pg * kPageBytes + sub * 1024), 16, 0, 0);
             }
         }
     };
-    auto store_tile = [&](int buf) {
+    // After this wave's loads of tile kt landed: value slots at or past the sequence
+    // end become 0 (masked keys get weight 0, and 0 * NaN would poison the product).
+    auto zero_tail = [&](unsigned char* vdst, int kt) {
+        const int first_bad = L - kt * kBlockN;  // tile-relative key index
+        if (first_bad >= kBlockN) return;
 #pragma unroll
-        for (int e = 0; e < NCH; ++e) {
-            const int p = e * kPagesPerPass + pip;
-            const int krow = p * kPage + k_slot;
-            *reinterpret_cast<u32x4*>(&k_lds[buf][krow * D + swz_k<D>(k_chunk, krow) * 8]) = kreg[e];
-            *reinterpret_cast<u32x4*>(&v_lds[buf][v_row * kBlockN + swz_v(2 * p + v_half, v_row) * 8]) = vreg[e];
+        for (int e = 0; e < NI; ++e) {
+            const int pg = page_of(e);
+            const int key0 = pg * kPage + v_half * 8;
+            uint16_t* dst = reinterpret_cast<uint16_t*>(vdst + pg * kPageBytes + sub * 1024 + lane * 16);
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                if (key0 + x >= first_bad) dst[x] = 0;
         }
     };
 
     f32x16 o[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[db] = f32x16{};
-    float m_run = -INFINITY;  // running row max of score * scale * log2(e)
-    float l_run = 0.f;        // this lane's half of the running row sum
+    float m_run = -INFINITY;  // max of score * scale * log2(e) used as the exponent offset
+    float l_run = 0.f;        // this lane's half of the row sum of the bf16 weights
     const float c = a.scale_log2;
     // key row fed to the QK^T product by this lane: bits 2 and 3 of lr swapped
     const int prow = (lr & 0x13) | ((lr & 4) << 1) | ((lr & 8) >> 1);
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-    int kt = it.kt_begin;
-    load_tile(kt);
-    store_tile(0);
-    __syncthreads();
-    for (int i = 0; kt < it.kt_end; ++kt, ++i) {
-        const int buf = i & 1;
-        const bool more = kt + 1 < it.kt_end;
-        if (more) load_tile(kt + 1);
-        const uint16_t* kb = k_lds[buf];
-        const uint16_t* vb = v_lds[buf];
-
+    auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt) {
         f32x16 s[2];
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
@@ -168,20 +174,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
             const int krow = 32 * b + prow;
 #pragma unroll
             for (int k = 0; k < DK; ++k) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + krow * D + swz_k<D>(2 * k + hh, krow) * 8);
+                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + krow * (2 * D) + swz_k<D>(2 * k + hh, krow) * 16);
                 s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], s[b], 0, 0, 0);
             }
         }
-        // s[b][e] is the score of key tile_base + 32b + 16(e>>3) + 8hh + (e&7)
+        // s[b][e] is the score of tile key 32b + 16(e>>3) + 8hh + (e&7)
         const int key0 = kt * kBlockN;
         if (key0 + kBlockN - 1 > P + it.q0) {
+            const int rel = lim - key0 - 8 * hh;
 #pragma unroll
             for (int b = 0; b < 2; ++b)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int key = key0 + 32 * b + 16 * (e >> 3) + 8 * hh + (e & 7);
-                    if (key > lim) s[b][e] = -INFINITY;
-                }
+                for (int e = 0; e < 16; ++e)
+                    if (32 * b + 16 * (e >> 3) + (e & 7) > rel) s[b][e] = -INFINITY;
         }
         float mx = -INFINITY;
 #pragma unroll
@@ -189,33 +194,73 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
 #pragma unroll
             for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[b][e]);
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx * c);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        m_run = m_new;
-        l_run *= alpha;
+        const float m_tile = mx * c;
+        if (__any(m_tile > m_run + kTileLog2Thresh)) {
+            const float m_new = fmaxf(m_run, m_tile);
+            // rows that have seen no visible key yet (all -inf; possible in a key chunk
+            // that starts past them) hold o = l = 0: any finite alpha keeps them so
+            const float alpha = m_new == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[db] *= alpha;
+            for (int db = 0; db < DB; ++db) o[db] *= alpha;
+        }
+        const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
 
         bf16x8 pf[4];
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(s[b][e], c, -m_use));
-                l_run += p;
-                pf[2 * b + (e >> 3)][e & 7] = (__bf16)p;
+            for (int e = 0; e < 16; ++e)
+                pf[2 * b + (e >> 3)][e & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[b][e], c, -m_use));
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                const bf16x2 pair = {pf[st][2 * x], pf[st][2 * x + 1]};
+                l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
             }
+        }
 #pragma unroll
         for (int st = 0; st < 4; ++st)
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
                 const int d = 32 * db + lr;
-                const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vb + d * kBlockN + swz_v(2 * st + hh, d) * 8);
+                const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
+                    vb + st * kPageBytes + d * 32 + ((hh ^ ((d >> 3) & 1)) * 16));
                 o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st], o[db], 0, 0, 0);
             }
-        if (more) store_tile(buf ^ 1);
+    };
+
+    // One pipeline step: start the next tile's loads into the other buffers, compute
+    // this tile, make the next tile visible.
+    int ids[4];
+    int kt = it.kt_begin;
+    auto step = [&](unsigned char* kc, unsigned char* vc, unsigned char* kn, unsigned char* vn) {
+        const bool more = kt + 1 < it.kt_end;
+        if (more) {
+            issue_tile(kn, vn, kt + 1, ids);
+            if (kt + 2 < it.kt_end) fetch_ids(kt + 2, ids);
+        }
+        compute_tile(kc, vc, kt);
+        if (more) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            zero_tail(vn, kt + 1);
+        }
         __syncthreads();
+    };
+
+    fetch_ids(kt, ids);
+    issue_tile(k_lds0, v_lds0, kt, ids);
+    if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    zero_tail(v_lds0, kt);
+    __syncthreads();
+    while (true) {
+        step(k_lds0, v_lds0, k_lds1, v_lds1);
+        if (++kt >= it.kt_end) break;
+        step(k_lds1, v_lds1, k_lds0, v_lds0);
+        if (++kt >= it.kt_end) break;
     }
 
     const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -258,9 +303,12 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
     constexpr int CPR = D / 4;  // float4 chunks per row
     const int kvh = (int)(blockIdx.x % (unsigned)a.num_kv_heads);
     const CombineItem ci = a.combines[blockIdx.x / (unsigned)a.num_kv_heads];
-    if (ci.ns <= 0) return;
+    if (ci.ns <= 0 || ci.r < 0 || ci.r >= a.batch || ci.q0 < 0 || ci.part_base < 0 ||
+        ci.part_base + ci.ns > a.num_partials)
+        return;
     const int cu = a.cu_new_lens[ci.r];
     const int n = a.cu_new_lens[ci.r + 1] - cu;
+    if (ci.q0 >= n) return;
     const int ntok = min(a.tq, n - ci.q0);
     const int rows = ntok * a.group;
     for (int x = threadIdx.x; x < rows * CPR; x += blockDim.x) {

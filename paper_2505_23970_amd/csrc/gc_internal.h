@@ -153,6 +153,7 @@ struct CombineArgs {
     const int32_t* cu_new_lens;
     const CombineItem* combines;
     int32_t num_q_heads, num_kv_heads, group, tq;
+    int32_t batch, num_partials;
 };
 
 hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s);

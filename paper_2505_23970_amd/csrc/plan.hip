@@ -3,24 +3,28 @@
 // captured in a graph).
 //
 // One workgroup:
-//   1. each thread counts the work items, split query tiles and partial slots
-//      of a contiguous range of requests, then an exclusive scan over threads
-//      gives every request its output offsets;
-//   2. items are emitted request-major (query tile, then key chunk), each split
-//      tile also emitting a merge entry with its partial slots;
-//   3. a counting sort by cost (key tiles) orders the list heaviest first, so
-//      the hardware dispatcher, which starts workgroups in index order, runs
-//      the longest items first (longest-processing-time scheduling).
+//   1. per-request query-tile counts and their exclusive scan (cum[], kept in
+//      the workspace), so that every thread can take query tiles of any request
+//      by a global tile index;
+//   2. a histogram of item costs (key tiles per item) in LDS, scanned so that
+//      the heaviest items come first;
+//   3. every item is written straight to its sorted position (an LDS cursor per
+//      cost bucket); split query tiles take their partial slots and merge entry
+//      from two LDS counters.
+// The hardware dispatcher starts workgroups in index order, so the longest
+// items start first (longest-processing-time scheduling). Order inside a cost
+// bucket and slot numbers may differ between runs; results do not depend on
+// them (every item writes its own outputs, merges run in chunk order).
 // If the device lengths do not reproduce the host's totals (the caller passed
 // different host and device arrays), every item is emitted empty and status[0]
-// is set to 1: the attention kernel then writes nothing, but never strays out
-// of bounds.
+// is set to 1: the attention kernel then writes nothing, and nothing is
+// accessed out of bounds.
 #include "gc_internal.h"
 
 namespace gc {
 namespace {
 
-// exclusive scan of one value per thread; returns the thread's offset, *total the sum
+// exclusive scan of one value per thread; *total receives the sum
 __device__ int block_exclusive_scan(int v, int* s_tmp, int* total) {
     const int tid = threadIdx.x;
     s_tmp[tid] = v;
@@ -37,81 +41,111 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int* total) {
     return incl - v;
 }
 
+__device__ __forceinline__ int bucket_of(int cost) {
+    return kCostBuckets - 1 - min(cost, kCostBuckets - 1);  // heaviest first
+}
+
+struct Tile {
+    int r, q0, kt, ns;
+};
+
+// query tile number g (over the whole batch) -> request, first token, key tiles, splits
+__device__ __forceinline__ Tile tile_at(const PlanArgs& a, const int* cum, int g) {
+    int lo = 0, hi = a.batch;  // largest r with cum[r] <= g
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (cum[mid] <= g) lo = mid;
+        else hi = mid;
+    }
+    Tile t;
+    t.r = lo;
+    t.q0 = (g - cum[lo]) * a.tq;
+    const int n = a.cu_new_lens[lo + 1] - a.cu_new_lens[lo];
+    const int ntok = min(a.tq, n - t.q0);
+    t.kt = key_tiles(a.prefix_lens[lo], t.q0, ntok);
+    t.ns = num_splits(t.kt, a.chunk);
+    return t;
+}
+
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
     __shared__ int s_tmp[kPlanThreads];
     __shared__ int s_hist[kCostBuckets];
+    __shared__ int s_part, s_comb, s_bad;
     const int tid = threadIdx.x;
+    int* cum = a.scratch;  // [batch + 1]
+
+    // 1. query tiles per request, scanned
     const int per = ceil_div(a.batch, kPlanThreads);
     const int r0 = min(a.batch, tid * per), r1 = min(a.batch, r0 + per);
-
-    int ni = 0, nc = 0, np = 0;
+    int mine = 0;
+    for (int r = r0; r < r1; ++r)
+        mine += ceil_div(a.cu_new_lens[r + 1] - a.cu_new_lens[r], a.tq);
+    int total_tiles;
+    int off = block_exclusive_scan(mine, s_tmp, &total_tiles);
     for (int r = r0; r < r1; ++r) {
-        const int n = a.cu_new_lens[r + 1] - a.cu_new_lens[r];
-        const RequestCounts c = request_counts(a.prefix_lens[r], n, a.tq, a.chunk);
-        ni += c.items;
-        nc += c.combines;
-        np += c.partials;
+        cum[r] = off;
+        off += ceil_div(a.cu_new_lens[r + 1] - a.cu_new_lens[r], a.tq);
     }
-    int ti, tc, tp;
-    int oi = block_exclusive_scan(ni, s_tmp, &ti);
-    int oc = block_exclusive_scan(nc, s_tmp, &tc);
-    int op = block_exclusive_scan(np, s_tmp, &tp);
-
-    if (ti != a.expect_items || tc != a.expect_combines || tp != a.expect_partials) {
-        for (int i = tid; i < a.expect_items; i += kPlanThreads)
-            a.items[i] = WorkItem{-1, 0, 0, 0, -1, 0, 0, 0};
-        for (int i = tid; i < a.expect_combines; i += kPlanThreads)
-            a.combines[i] = CombineItem{0, 0, 0, 0};
-        if (tid == 0) a.status[0] = 1;
-        return;
-    }
-
-    for (int r = r0; r < r1; ++r) {
-        const int P = a.prefix_lens[r];
-        const int n = a.cu_new_lens[r + 1] - a.cu_new_lens[r];
-        for (int q0 = 0; q0 < n; q0 += a.tq) {
-            const int ntok = min(a.tq, n - q0);
-            const int kt = key_tiles(P, q0, ntok);
-            const int ns = num_splits(kt, a.chunk);
-            if (ns == 1) {
-                a.unsorted[oi++] = WorkItem{r, q0, 0, kt, -1, 0, 0, 0};
-            } else {
-                a.combines[oc++] = CombineItem{r, q0, op, ns};
-                for (int s = 0; s < ns; ++s)
-                    a.unsorted[oi++] = WorkItem{r, q0, split_begin(s, kt, ns), split_begin(s + 1, kt, ns), op + s, 0, 0, 0};
-                op += ns;
-            }
-        }
-    }
-
-    // counting sort, heaviest first: bucket kCostBuckets-1-cost
+    if (tid == 0) cum[a.batch] = total_tiles;
     for (int b = tid; b < kCostBuckets; b += kPlanThreads) s_hist[b] = 0;
+    if (tid == 0) {
+        s_part = 0;
+        s_comb = 0;
+        s_bad = 0;
+    }
     __threadfence_block();
     __syncthreads();
-    for (int i = tid; i < ti; i += kPlanThreads) {
-        const WorkItem w = a.unsorted[i];
-        const int cost = min(w.kt_end - w.kt_begin, kCostBuckets - 1);
-        atomicAdd(&s_hist[kCostBuckets - 1 - cost], 1);
+
+    // 2. cost histogram
+    for (int g = tid; g < total_tiles; g += kPlanThreads) {
+        const Tile t = tile_at(a, cum, g);
+        for (int s = 0; s < t.ns; ++s)
+            atomicAdd(&s_hist[bucket_of(split_begin(s + 1, t.kt, t.ns) - split_begin(s, t.kt, t.ns))], 1);
     }
     __syncthreads();
     constexpr int kPer = kCostBuckets / kPlanThreads;
     int local = 0;
     for (int k = 0; k < kPer; ++k) local += s_hist[tid * kPer + k];
-    int dummy;
-    int base = block_exclusive_scan(local, s_tmp, &dummy);
+    int total_items;
+    int base = block_exclusive_scan(local, s_tmp, &total_items);
     for (int k = 0; k < kPer; ++k) {
         const int c = s_hist[tid * kPer + k];
         s_hist[tid * kPer + k] = base;
         base += c;
     }
+    // merge entries start empty; the split tiles below fill theirs
+    for (int i = tid; i < a.expect_combines; i += kPlanThreads) a.combines[i] = CombineItem{0, 0, 0, 0};
     __syncthreads();
-    for (int i = tid; i < ti; i += kPlanThreads) {
-        const WorkItem w = a.unsorted[i];
-        const int cost = min(w.kt_end - w.kt_begin, kCostBuckets - 1);
-        const int pos = atomicAdd(&s_hist[kCostBuckets - 1 - cost], 1);
-        a.items[pos] = w;
+    if (total_items != a.expect_items) {
+        for (int i = tid; i < a.expect_items; i += kPlanThreads)
+            a.items[i] = WorkItem{-1, 0, 0, 0, -1, 0, 0, 0};
+        if (tid == 0) a.status[0] = 1;
+        return;
     }
-    if (tid == 0) a.status[0] = 0;
+
+    // 3. items at their sorted positions
+    for (int g = tid; g < total_tiles; g += kPlanThreads) {
+        const Tile t = tile_at(a, cum, g);
+        int part0 = -1;
+        if (t.ns > 1) {
+            part0 = atomicAdd(&s_part, t.ns);
+            const int ci = atomicAdd(&s_comb, 1);
+            if (part0 + t.ns > a.expect_partials || ci >= a.expect_combines) {
+                s_bad = 1;  // cannot happen when the item totals matched; never write out of range
+                part0 = -2;
+            } else {
+                a.combines[ci] = CombineItem{t.r, t.q0, part0, t.ns};
+            }
+        }
+        for (int s = 0; s < t.ns; ++s) {
+            const int b0 = split_begin(s, t.kt, t.ns), b1 = split_begin(s + 1, t.kt, t.ns);
+            const int pos = atomicAdd(&s_hist[bucket_of(b1 - b0)], 1);
+            a.items[pos] = part0 == -2 ? WorkItem{-1, 0, 0, 0, -1, 0, 0, 0}
+                                       : WorkItem{t.r, t.q0, b0, b1, part0 < 0 ? -1 : part0 + s, 0, 0, 0};
+        }
+    }
+    __syncthreads();
+    if (tid == 0) a.status[0] = s_bad;
 }
 
 }  // namespace

@@ -107,8 +107,11 @@ def compare_attention(w: W.Workload, out_dev, lse_dev, ref_out, ref_lse, rows=No
     if contract:
         assert info["max_abs"] <= CONTRACT_MAX_ABS and info["mean_abs"] <= CONTRACT_MEAN_ABS, info
     if got_lse is not None and ref_lse is not None:
+        # the kernel's normaliser is the sum of the bf16-rounded weights (the same
+        # weights that enter the PV product), within a factor 1 +- 2^-8 of the exact
+        # sum, so ln of it is within 2^-8; fp32 terms add ~1e-5 relative
         lerr = np.abs(got_lse - ref_lse)
-        assert np.all(lerr <= 1e-4 + 1e-5 * np.abs(ref_lse)), f"lse error {lerr.max()}"
+        assert np.all(lerr <= 2.0 ** -8 + 1e-5 * np.abs(ref_lse)), f"lse error {lerr.max()}"
         info["lse_max_abs"] = float(lerr.max(initial=0.0))
     return info
 
