@@ -78,6 +78,26 @@ def copy_reference(mib):
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}), flush=True)
 
 
+def profiled_traffic(workload):
+    """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary of this workload, if it was taken on the current kernel source; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attention_{workload}.md")
+    src = os.path.join(ROOT, "paper_2505_23970_amd", "csrc", "attention.hip")
+    if not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-json:"):
+                rec = json.loads(line.split(":", 1)[1])
+    if rec is None:
+        return None
+    with open(src, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    return rec["traffic_bytes"] if rec.get("kernel_source_sha256_16") == sha else None
+
+
 def cpu_oracle_baseline(w, target_s):
     """Time the fp64 oracle on a bounded sample of the workload's output rows."""
     import oracle
@@ -196,7 +216,8 @@ def main():
                       "attention_p90": float(np.percentile(att, 90))},
         "algorithmic": {"flops": F, "attn_bytes": w.attn_bytes(), "append_bytes": w.append_bytes()},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": profiled_traffic(w.name),
                      "kernel": "attention_kernel<128> (+ split merge when the plan splits)",
                      "hbm_gbs_algorithmic": w.attn_bytes() / t_att / 1e9},
     }
