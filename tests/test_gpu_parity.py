@@ -132,6 +132,21 @@ def test_position_code_window(split):
             assert np.all(got[cu[r] + i] == expect), (r, i, got[cu[r] + i], expect)
 
 
+@pytest.mark.parametrize("split", [None, 1])
+def test_score_jump_beyond_offset_slack(split):
+    """A key whose score exceeds the earlier ones by ~130 in log2 units (more than the
+    kernel's 2^64 offset slack): the exponent offset set by the first tile is too small
+    and the work item must be redone with the larger one (fp32 would overflow otherwise)."""
+    w = W.build([300, 70], [40, 9], 8, 1, 128, seed=104, name="score_jump")
+    w.q[:, :, 0] = W.f32_to_bf16_bits(np.float32(8.0))
+    w.k_prefix[250, :, 0] = W.f32_to_bf16_bits(np.float32(128.0))  # request 0, position 250
+    w.finish()
+    _, _, out = full_check(w, kv_split_tiles=split)
+    vpre = W.bf16_bits_to_f32(w.v_prefix).astype(np.float64)
+    got = H.from_dev_f32(out)
+    np.testing.assert_allclose(got[:40, 0], np.broadcast_to(vpre[250, 0], (40, 128)), atol=2e-2)
+
+
 # ----------------------------------------------------------------- edge cases
 
 EDGES = [
