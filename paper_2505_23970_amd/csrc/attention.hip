@@ -22,6 +22,10 @@
 // global loads are in flight while the current tile is computed. Value pages
 // are stored transposed in the pool ([D][16]), so both LDS tiles are read with
 // 16-byte loads; XOR swizzles keep those reads free of bank conflicts.
+// The tile copies go straight from global memory to LDS; they are issued as
+// inline assembly with explicit waits, so the compiler's own LDS waits count
+// only LDS reads and can keep several fragment reads in flight per MFMA
+// (scheduling fences hold that order).
 #include "gc_internal.h"
 
 namespace gc {
@@ -49,9 +53,30 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-// Uniform loads through the constant address space become scalar loads.
-typedef const __attribute__((address_space(4))) int32_t* scalar_i32p;
-typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// A direct global->LDS copy of 16 bytes per lane: lane i's bytes land at
+// lds_dst + 16 i (lds_dst is wave-uniform). Issued as inline assembly so the
+// compiler does not track it: every wait for these copies is explicit (wait_vmem).
+// The compiler emits no other use of m0 in these kernels; the clobber keeps it that way.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* gsrc, const unsigned char* lds_dst) {
+    const uint32_t l = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char*)lds_dst);
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :: "v"(gsrc), "s"(l) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (s_waitcnt immediate: vmcnt in bits 3:0, expcnt 6:4 and lgkmcnt 11:8 left at
+// their maxima). A real wait instruction, so the compiler also knows it.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N < 16, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+    asm volatile("" ::: "memory");  // no LDS access moves above the wait
+}
 
 template <int D>
 __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnArgs a) {
@@ -110,33 +135,35 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
     // Direct global->LDS loads: instruction e of a wave moves 1 KiB piece 4e + wave of
     // a tile tensor, i.e. piece `sub` of page `page_of(e)`; lane i lands at byte 16 i.
     const int sub = wave % kKbPerPage;
-    auto page_of = [&](int e) -> int { return kKbPerPage == 4 ? e : (4 * e + wave) / kKbPerPage; };
+    static_assert(kWaves % kKbPerPage == 0, "piece layout");
+    auto page_of = [&](int e) -> int { return (kWaves * e + wave) / kKbPerPage; };
     const int k_row = sub * (1024 / (2 * D)) + lane / (D / 8);         // key slot in the page
     const uint32_t k_src = k_row * (2 * D) + swz_k<D>(lane % (D / 8), k_row) * 16;
     const int v_d = sub * 32 + (lane >> 1);                            // value row (d) in the page
     const int v_half = (lane & 1) ^ ((v_d >> 3) & 1);                  // logical half held by the lane
     const uint32_t v_src = v_d * 32 + v_half * 16;
-    const scalar_i32p table = (scalar_i32p)(a.block_tables + (int64_t)r * a.max_blocks);
+    const int32_t* table = a.block_tables + (int64_t)r * a.max_blocks;
     const int64_t head_off = (int64_t)kvh * kPageBytes;
     const int64_t block_stride = (int64_t)a.num_kv_heads * kPageBytes;
 
     // raw table entries of tile kt (indices clamped into the row; checked at use)
-    auto fetch_ids = [&](int kt, int (&ids)[4]) {
-#pragma unroll
-        for (int p = 0; p < 4; ++p) ids[p] = table[min(kt * 4 + p, a.max_blocks - 1)];
+    // (a vector load: lane p of every 4 holds entry p; it completes with the tile loads,
+    // and no scalar load is left in flight to force full LDS waits in the compute phase)
+    auto fetch_ids = [&](int kt, int& ids) {
+        ids = table[min(kt * 4 + (lane & 3), a.max_blocks - 1)];
     };
-    auto issue_tile = [&](unsigned char* kdst, unsigned char* vdst, int kt, const int (&ids)[4]) {
+    auto issue_tile = [&](unsigned char* kdst, unsigned char* vdst, int kt, const int ids) {
 #pragma unroll
         for (int e = 0; e < NI; ++e) {
             const int pg = page_of(e);
             const int lp = kt * 4 + pg;
-            const int blk = ids[pg];
+            const int blk = __builtin_amdgcn_readlane(ids, pg);
             if (lp < a.max_blocks && lp * kPage < L && blk >= 0 && blk < a.num_blocks) {
                 const int64_t base = (int64_t)blk * block_stride + head_off;
                 const unsigned char* kg = reinterpret_cast<const unsigned char*>(a.k_pool) + base;
                 const unsigned char* vg = reinterpret_cast<const unsigned char*>(a.v_pool) + base;
-                __builtin_amdgcn_global_load_lds(kg + k_src, (lds_ptr)(kdst + pg * kPageBytes + sub * 1024), 16, 0, 0);
-                __builtin_amdgcn_global_load_lds(vg + v_src, (lds_ptr)(vdst + pg * kPageBytes + sub * 1024), 16, 0, 0);
+                dma16(kg + k_src, kdst + pg * kPageBytes + sub * 1024);
+                dma16(vg + v_src, vdst + pg * kPageBytes + sub * 1024);
             }
         }
     };
@@ -166,18 +193,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
     const int prow = (lr & 0x13) | ((lr & 4) << 1) | ((lr & 8) >> 1);
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
+    constexpr int kAhead = 6;  // LDS fragment reads kept in flight ahead of their MFMA
     auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt) {
-        f32x16 s[2];
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            s[b] = f32x16{};
+        // S^T = K_tile . Q^T: MFMA i uses K fragment (k = i/2, block b = i%2). Every
+        // group below is fenced so the fragment reads stay kAhead MFMAs ahead.
+        bf16x8 kf[2 * DK];
+        auto kread = [&](int i) {
+            const int k = i >> 1, b = i & 1;
             const int krow = 32 * b + prow;
+            kf[i] = *reinterpret_cast<const bf16x8*>(kb + krow * (2 * D) + swz_k<D>(2 * k + hh, krow) * 16);
+        };
+        f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-            for (int k = 0; k < DK; ++k) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kb + krow * (2 * D) + swz_k<D>(2 * k + hh, krow) * 16);
-                s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], s[b], 0, 0, 0);
-            }
+        for (int i = 0; i < kAhead; ++i) kread(i);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 2 * DK; ++i) {
+            if (i + kAhead < 2 * DK) kread(i + kAhead);
+            s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[i >> 1], s[i & 1], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
+        // V fragments of the first value page go out now; they land during the softmax
+        bf16x8 vf[4 * DB];
+        auto vread = [&](int i) {
+            const int st = i / DB, db = i % DB;
+            const int d = 32 * db + lr;
+            vf[i] = *reinterpret_cast<const bf16x8*>(vb + st * kPageBytes + d * 32 + ((hh ^ ((d >> 3) & 1)) * 16));
+        };
+#pragma unroll
+        for (int i = 0; i < kAhead; ++i) vread(i);
+        __builtin_amdgcn_sched_barrier(0);
+
         // s[b][e] is the score of tile key 32b + 16(e>>3) + 8hh + (e&7)
         const int key0 = kt * kBlockN;
         if (key0 + kBlockN - 1 > P + it.q0) {
@@ -186,14 +232,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
             for (int b = 0; b < 2; ++b)
 #pragma unroll
                 for (int e = 0; e < 16; ++e)
-                    if (32 * b + 16 * (e >> 3) + (e & 7) > rel) s[b][e] = -INFINITY;
+                    s[b][e] = (32 * b + 16 * (e >> 3) + (e & 7) > rel) ? -INFINITY : s[b][e];
         }
-        float mx = -INFINITY;
+        // tree maximum, then the other half of the lane pair
+        float t8[8];
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int x = 0; x < 8; ++x)
+            t8[x] = fmaxf(fmaxf(s[0][2 * x], s[0][2 * x + 1]), fmaxf(s[1][2 * x], s[1][2 * x + 1]));
 #pragma unroll
-            for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[b][e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        for (int x = 0; x < 4; ++x) t8[x] = fmaxf(t8[x], t8[x + 4]);
+        float mx = fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3]));
+        {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+            mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+        }
         const float m_tile = mx * c;
         if (__any(m_tile > m_run + kTileLog2Thresh)) {
             const float m_new = fmaxf(m_run, m_tile);
@@ -206,35 +258,43 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
         }
         const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+        __builtin_amdgcn_sched_barrier(0);
 
+        // O^T += V^T . P^T, one 16-key step st at a time: the weights of step st are
+        // computed, then its DB MFMAs are issued while the next step's weights compute.
         bf16x8 pf[4];
+        auto weights = [&](int st) {
+            const int b = st >> 1, e0 = (st & 1) * 8;
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                pf[2 * b + (e >> 3)][e & 7] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[b][e], c, -m_use));
-#pragma unroll
-        for (int st = 0; st < 4; ++st) {
+            for (int e = 0; e < 8; ++e)
+                pf[st][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[b][e0 + e], c, -m_use));
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
                 const bf16x2 pair = {pf[st][2 * x], pf[st][2 * x + 1]};
                 l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
             }
-        }
+        };
+        weights(0);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int st = 0; st < 4; ++st)
+        for (int st = 0; st < 4; ++st) {
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                const int d = 32 * db + lr;
-                const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
-                    vb + st * kPageBytes + d * 32 + ((hh ^ ((d >> 3) & 1)) * 16));
-                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st], o[db], 0, 0, 0);
+                const int i = st * DB + db;
+                if (i + kAhead < 4 * DB) vread(i + kAhead);
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pf[st], o[db], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
+            if (st + 1 < 4) {
+                weights(st + 1);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
     };
 
     // One pipeline step: start the next tile's loads into the other buffers, compute
     // this tile, make the next tile visible.
-    int ids[4];
+    int ids;
     int kt = it.kt_begin;
     auto step = [&](unsigned char* kc, unsigned char* vc, unsigned char* kn, unsigned char* vn) {
         const bool more = kt + 1 < it.kt_end;
@@ -244,7 +304,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
         }
         compute_tile(kc, vc, kt);
         if (more) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            wait_vmem<0>();
             zero_tail(vn, kt + 1);
         }
         __syncthreads();
@@ -253,7 +313,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
     fetch_ids(kt, ids);
     issue_tile(k_lds0, v_lds0, kt, ids);
     if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wait_vmem<0>();
     zero_tail(v_lds0, kt);
     __syncthreads();
     while (true) {
