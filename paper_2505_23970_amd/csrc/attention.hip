@@ -358,11 +358,20 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
 
 // Merge the key chunks of one split query tile: lse = log sum_s exp(lse_s),
 // o = sum_s exp(lse_s - lse) o_s, in a fixed chunk order (deterministic).
+// A workgroup merges kCombineRows rows of one (query tile, KV head); a thread
+// owns four consecutive output elements of one row, so the partial rows are
+// read with coalesced 16-byte loads.
 template <int D>
-__global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
-    constexpr int CPR = D / 4;  // float4 chunks per row
-    const int kvh = (int)(blockIdx.x % (unsigned)a.num_kv_heads);
-    const CombineItem ci = a.combines[blockIdx.x / (unsigned)a.num_kv_heads];
+__global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineArgs a) {
+    constexpr int CPR = D / 4;                      // float4 chunks per row
+    constexpr int kRows = kCombineThreads / CPR;    // rows per workgroup
+    static_assert(kBlockM % kRows == 0, "row groups");
+    constexpr int kGroups = kBlockM / kRows;
+    const unsigned tile = blockIdx.x / kGroups;
+    const int m = (int)(blockIdx.x % kGroups) * kRows + (int)threadIdx.x / CPR;
+    const int c4 = (int)threadIdx.x % CPR;
+    const int kvh = (int)(tile % (unsigned)a.num_kv_heads);
+    const CombineItem ci = a.combines[tile / (unsigned)a.num_kv_heads];
     if (ci.ns <= 0 || ci.r < 0 || ci.r >= a.batch || ci.q0 < 0 || ci.part_base < 0 ||
         ci.part_base + ci.ns > a.num_partials)
         return;
@@ -370,31 +379,28 @@ __global__ __launch_bounds__(256) void combine_kernel(const CombineArgs a) {
     const int n = a.cu_new_lens[ci.r + 1] - cu;
     if (ci.q0 >= n) return;
     const int ntok = min(a.tq, n - ci.q0);
-    const int rows = ntok * a.group;
-    for (int x = threadIdx.x; x < rows * CPR; x += blockDim.x) {
-        const int m = x / CPR, c4 = x % CPR;
-        const int t = m / a.group, hl = m - t * a.group;
-        float mx = -INFINITY;
-        for (int s = 0; s < ci.ns; ++s)
-            mx = fmaxf(mx, a.part_lse[((int64_t)(ci.part_base + s) * a.num_kv_heads + kvh) * kBlockM + m]);
-        float tot = 0.f;
-        for (int s = 0; s < ci.ns; ++s)
-            tot += expf(a.part_lse[((int64_t)(ci.part_base + s) * a.num_kv_heads + kvh) * kBlockM + m] - mx);
-        const float lse_tot = mx + logf(tot);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < ci.ns; ++s) {
-            const int64_t pr = ((int64_t)(ci.part_base + s) * a.num_kv_heads + kvh) * kBlockM + m;
-            const float w = expf(a.part_lse[pr] - lse_tot);
-            const f32x4 v = *reinterpret_cast<const f32x4*>(a.part_o + pr * D + 4 * c4);
-            acc += w * v;
-        }
-        const int64_t qrow = (int64_t)(cu + ci.q0 + t) * a.num_q_heads + kvh * a.group + hl;
-        u32x2 w2;
-        w2[0] = pack_bf16x2(acc[0], acc[1]);
-        w2[1] = pack_bf16x2(acc[2], acc[3]);
-        *reinterpret_cast<u32x2*>(a.out + qrow * D + 4 * c4) = w2;
-        if (a.lse != nullptr && c4 == 0) a.lse[qrow] = lse_tot;
+    const int t = m / a.group, hl = m - t * a.group;
+    if (t >= ntok) return;
+    const int64_t row0 = ((int64_t)ci.part_base * a.num_kv_heads + kvh) * kBlockM + m;
+    const int64_t split_stride = (int64_t)a.num_kv_heads * kBlockM;  // rows between chunks
+    float mx = -INFINITY;
+    for (int s = 0; s < ci.ns; ++s) mx = fmaxf(mx, a.part_lse[row0 + s * split_stride]);
+    float tot = 0.f;
+    for (int s = 0; s < ci.ns; ++s) tot += expf(a.part_lse[row0 + s * split_stride] - mx);
+    const float lse_tot = mx + logf(tot);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ci.ns; ++s) {
+        const int64_t pr = row0 + s * split_stride;
+        const float w = expf(a.part_lse[pr] - lse_tot);
+        const f32x4 v = *reinterpret_cast<const f32x4*>(a.part_o + pr * D + 4 * c4);
+        acc += w * v;
     }
+    const int64_t qrow = (int64_t)(cu + ci.q0 + t) * a.num_q_heads + kvh * a.group + hl;
+    u32x2 w2;
+    w2[0] = pack_bf16x2(acc[0], acc[1]);
+    w2[1] = pack_bf16x2(acc[2], acc[3]);
+    *reinterpret_cast<u32x2*>(a.out + qrow * D + 4 * c4) = w2;
+    if (a.lse != nullptr && c4 == 0) a.lse[qrow] = lse_tot;
 }
 
 }  // namespace
@@ -409,11 +415,12 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, 
 }
 
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s) {
-    const dim3 grid((unsigned)(num_combines * a.num_kv_heads));
+    const int groups = kBlockM / (kCombineThreads / (head_dim / 4));
+    const dim3 grid((unsigned)(num_combines * a.num_kv_heads * groups));
     if (head_dim == 128)
-        combine_kernel<128><<<grid, 256, 0, s>>>(a);
+        combine_kernel<128><<<grid, kCombineThreads, 0, s>>>(a);
     else
-        combine_kernel<64><<<grid, 256, 0, s>>>(a);
+        combine_kernel<64><<<grid, kCombineThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 
