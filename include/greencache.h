@@ -61,7 +61,7 @@ typedef enum gc_status {
     GC_OK = 0,
     GC_ERR_NULL_ARG = -1,    /* a required pointer is NULL */
     GC_ERR_BAD_SHAPE = -2,   /* negative length, Hq % Hkv != 0, non-positive sizes, bad scale */
-    GC_ERR_UNSUPPORTED = -3, /* head_dim not 64/128, page_size != 16, Hq/Hkv > 128 */
+    GC_ERR_UNSUPPORTED = -3, /* head_dim not 64/128, page_size != 16, Hq/Hkv > 128, Hkv > 65535 */
     GC_ERR_BLOCK_TABLE = -4, /* ceil((P_r + n_r) / page_size) > max_blocks_per_seq */
     GC_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required */
     GC_ERR_HIP = -6          /* a HIP launch or runtime call failed */

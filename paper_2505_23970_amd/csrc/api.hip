@@ -33,6 +33,7 @@ gc_status check_common(const gc_geometry* geo, const gc_batch* b, Shape* sh) {
     if (geo->num_q_heads % geo->num_kv_heads != 0) return GC_ERR_BAD_SHAPE;
     const int group = geo->num_q_heads / geo->num_kv_heads;
     if (group > gc::kBlockM) return GC_ERR_UNSUPPORTED;
+    if (geo->num_kv_heads > 65535) return GC_ERR_UNSUPPORTED;  // append grid dimension
     if (geo->head_dim != 64 && geo->head_dim != 128) return GC_ERR_UNSUPPORTED;
     if (geo->page_size != gc::kPage) return GC_ERR_UNSUPPORTED;
     sh->group = group;

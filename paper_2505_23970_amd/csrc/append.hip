@@ -2,8 +2,9 @@
 // (GreenCache §2.2, Fig. 1a step 1: the processed request's KV is saved so a
 // later request with the same context can reuse it).
 //
-// A workgroup takes 16 consecutive packed new tokens and walks the KV heads.
-// Keys are copied row by row (each 16-byte chunk read once, written once,
+// A workgroup takes 16 consecutive packed new tokens of one KV head (the grid
+// covers tokens x heads, so a batch of a few thousand tokens still fills the
+// GPU). Keys are copied row by row (each 16-byte chunk read once, written once,
 // coalesced on both sides). Values go to transposed pages ([D][16]): the 16
 // tokens' rows are staged in LDS and written out column-wise, so the 16 lanes
 // that write one page row touch 32 consecutive bytes when the tokens share a
@@ -51,36 +52,34 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendArgs
     }
     __syncthreads();
 
-    for (int h = 0; h < a.num_kv_heads; ++h) {
-        for (int x = tid; x < kAppendTokens * CPR; x += kAppendThreads) {
-            const int tl = x / CPR, ch = x % CPR;
-            u32x4 v = u32x4{0u, 0u, 0u, 0u};
-            if (tl < ntok) {
-                const int64_t src = ((int64_t)(tok0 + tl) * a.num_kv_heads + h) * D + ch * 8;
-                const int blk = s_blk[tl];
-                if (blk >= 0) {
-                    const u32x4 k = *reinterpret_cast<const u32x4*>(a.k_new + src);
-                    *reinterpret_cast<u32x4*>(a.k_pool + (((int64_t)blk * a.num_kv_heads + h) * kPage + s_off[tl]) * D + ch * 8) = k;
-                }
-                v = *reinterpret_cast<const u32x4*>(a.v_new + src);
-            }
-            *reinterpret_cast<u32x4*>(&s_v[tl * kStride + ch * 8]) = v;
-        }
-        __syncthreads();
-        for (int x = tid; x < kAppendTokens * D; x += kAppendThreads) {
-            const int tl = x % kAppendTokens, d = x / kAppendTokens;
+    const int h = blockIdx.y;
+    for (int x = tid; x < kAppendTokens * CPR; x += kAppendThreads) {
+        const int tl = x / CPR, ch = x % CPR;
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if (tl < ntok) {
+            const int64_t src = ((int64_t)(tok0 + tl) * a.num_kv_heads + h) * D + ch * 8;
             const int blk = s_blk[tl];
-            if (tl < ntok && blk >= 0)
-                a.v_pool[(((int64_t)blk * a.num_kv_heads + h) * D + d) * kPage + s_off[tl]] = s_v[tl * kStride + d];
+            if (blk >= 0) {
+                const u32x4 k = *reinterpret_cast<const u32x4*>(a.k_new + src);
+                *reinterpret_cast<u32x4*>(a.k_pool + (((int64_t)blk * a.num_kv_heads + h) * kPage + s_off[tl]) * D + ch * 8) = k;
+            }
+            v = *reinterpret_cast<const u32x4*>(a.v_new + src);
         }
-        __syncthreads();
+        *reinterpret_cast<u32x4*>(&s_v[tl * kStride + ch * 8]) = v;
+    }
+    __syncthreads();
+    for (int x = tid; x < kAppendTokens * D; x += kAppendThreads) {
+        const int tl = x % kAppendTokens, d = x / kAppendTokens;
+        const int blk = s_blk[tl];
+        if (tl < ntok && blk >= 0)
+            a.v_pool[(((int64_t)blk * a.num_kv_heads + h) * D + d) * kPage + s_off[tl]] = s_v[tl * kStride + d];
     }
 }
 
 }  // namespace
 
 hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s) {
-    const dim3 grid((unsigned)ceil_div(a.total_tokens, kAppendTokens));
+    const dim3 grid((unsigned)ceil_div(a.total_tokens, kAppendTokens), (unsigned)a.num_kv_heads);
     if (head_dim == 128)
         append_kernel<128><<<grid, kAppendThreads, 0, s>>>(a);
     else

@@ -20,6 +20,7 @@ constexpr int kAppendTokens = 16;  // new tokens per append workgroup
 constexpr int kAppendThreads = 256;
 constexpr int kCostBuckets = 2048;  // counting-sort buckets of the work list (cost in tiles)
 constexpr int kCombineThreads = 256;  // threads per split-merge workgroup
+constexpr int kPlanLdsBatch = 2048;   // batches up to this size are planned from LDS copies
 
 // One attention work item: query tile [q0, q0 + tq) of request r against key
 // tiles [kt_begin, kt_end). part >= 0 marks a split item whose normalised

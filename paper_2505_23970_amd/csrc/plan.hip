@@ -3,9 +3,10 @@
 // captured in a graph).
 //
 // One workgroup:
-//   1. per-request query-tile counts and their exclusive scan (cum[], kept in
-//      the workspace), so that every thread can take query tiles of any request
-//      by a global tile index;
+//   1. per-request query-tile counts and their exclusive scan (cum[], in LDS
+//      with the batch lengths for batches of up to kPlanLdsBatch requests, else
+//      in the workspace), so that every thread can take query tiles of any
+//      request by a global tile index;
 //   2. a histogram of item costs (key tiles per item) in LDS, scanned so that
 //      the heaviest items come first;
 //   3. every item is written straight to its sorted position (an LDS cursor per
@@ -49,20 +50,29 @@ struct Tile {
     int r, q0, kt, ns;
 };
 
+// Batch lengths as the planner reads them: LDS copies for batches of up to
+// kPlanLdsBatch requests (the searches below then cost no memory round trips),
+// else the global arrays.
+struct Lens {
+    const int* cum;     // [batch + 1] exclusive scan of query tiles per request
+    const int* cu;      // [batch + 1] exclusive scan of new tokens
+    const int* prefix;  // [batch]
+};
+
 // query tile number g (over the whole batch) -> request, first token, key tiles, splits
-__device__ __forceinline__ Tile tile_at(const PlanArgs& a, const int* cum, int g) {
+__device__ __forceinline__ Tile tile_at(const PlanArgs& a, const Lens& l, int g) {
     int lo = 0, hi = a.batch;  // largest r with cum[r] <= g
     while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (cum[mid] <= g) lo = mid;
+        if (l.cum[mid] <= g) lo = mid;
         else hi = mid;
     }
     Tile t;
     t.r = lo;
-    t.q0 = (g - cum[lo]) * a.tq;
-    const int n = a.cu_new_lens[lo + 1] - a.cu_new_lens[lo];
+    t.q0 = (g - l.cum[lo]) * a.tq;
+    const int n = l.cu[lo + 1] - l.cu[lo];
     const int ntok = min(a.tq, n - t.q0);
-    t.kt = key_tiles(a.prefix_lens[lo], t.q0, ntok);
+    t.kt = key_tiles(l.prefix[lo], t.q0, ntok);
     t.ns = num_splits(t.kt, a.chunk);
     return t;
 }
@@ -71,20 +81,30 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
     __shared__ int s_tmp[kPlanThreads];
     __shared__ int s_hist[kCostBuckets];
     __shared__ int s_part, s_comb, s_bad;
+    __shared__ int s_cum[kPlanLdsBatch + 1], s_cu[kPlanLdsBatch + 1], s_pre[kPlanLdsBatch];
     const int tid = threadIdx.x;
-    int* cum = a.scratch;  // [batch + 1]
+    const bool small = a.batch <= kPlanLdsBatch;
+    int* cum = small ? s_cum : a.scratch;  // [batch + 1]
+    if (small) {
+        for (int r = tid; r <= a.batch; r += kPlanThreads) {
+            s_cu[r] = a.cu_new_lens[r];
+            if (r < a.batch) s_pre[r] = a.prefix_lens[r];
+        }
+        __syncthreads();
+    }
+    const Lens lens{cum, small ? s_cu : a.cu_new_lens, small ? s_pre : a.prefix_lens};
 
     // 1. query tiles per request, scanned
     const int per = ceil_div(a.batch, kPlanThreads);
     const int r0 = min(a.batch, tid * per), r1 = min(a.batch, r0 + per);
     int mine = 0;
     for (int r = r0; r < r1; ++r)
-        mine += ceil_div(a.cu_new_lens[r + 1] - a.cu_new_lens[r], a.tq);
+        mine += ceil_div(lens.cu[r + 1] - lens.cu[r], a.tq);
     int total_tiles;
     int off = block_exclusive_scan(mine, s_tmp, &total_tiles);
     for (int r = r0; r < r1; ++r) {
         cum[r] = off;
-        off += ceil_div(a.cu_new_lens[r + 1] - a.cu_new_lens[r], a.tq);
+        off += ceil_div(lens.cu[r + 1] - lens.cu[r], a.tq);
     }
     if (tid == 0) cum[a.batch] = total_tiles;
     for (int b = tid; b < kCostBuckets; b += kPlanThreads) s_hist[b] = 0;
@@ -98,7 +118,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
 
     // 2. cost histogram
     for (int g = tid; g < total_tiles; g += kPlanThreads) {
-        const Tile t = tile_at(a, cum, g);
+        const Tile t = tile_at(a, lens, g);
         for (int s = 0; s < t.ns; ++s)
             atomicAdd(&s_hist[bucket_of(split_begin(s + 1, t.kt, t.ns) - split_begin(s, t.kt, t.ns))], 1);
     }
@@ -125,7 +145,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
 
     // 3. items at their sorted positions
     for (int g = tid; g < total_tiles; g += kPlanThreads) {
-        const Tile t = tile_at(a, cum, g);
+        const Tile t = tile_at(a, lens, g);
         int part0 = -1;
         if (t.ns > 1) {
             part0 = atomicAdd(&s_part, t.ns);

@@ -171,6 +171,17 @@ def test_edge_cases(name, P, n, Hq, Hkv, D):
     full_check(w, kv_split_tiles=1)
 
 
+def test_batch_beyond_lds_plan_limit():
+    """More requests than the planner keeps in LDS (2048): the work list is built
+    from the global length arrays instead."""
+    rng = np.random.default_rng(7)
+    P = rng.integers(0, 48, 2100).tolist()
+    n = rng.integers(0, 4, 2100).tolist()
+    w = W.build(P, n, 4, 1, 64, seed=260, values="unit", name="batch2100")
+    full_check(w)
+    full_check(w, kv_split_tiles=1)
+
+
 def test_longest_prefix_sampled():
     w = W.build([200_000], [40], 8, 1, 128, seed=250, name="longest")
     rows = np.array([0, 7, 8 * 20 + 3, 8 * 39, 8 * 39 + 7], np.int64)
