@@ -263,6 +263,17 @@ def short_suffix_variant(seed: int | None = None, new_tokens: int = 16) -> Workl
                  name=f"long_reuse_70b_n{new_tokens}")
 
 
+def decode_variant(seed: int | None = None, batch: int = 32) -> Workload:
+    """Decode step at the 70B shape: one new token per request over a cached context
+    (prefix lengths lognormal around 4096, clipped to [256, 32768]); K/V-read bound."""
+    if seed is None:
+        seed = SEED_BASE + 50
+    rng = np.random.default_rng(seed)
+    P = np.clip(np.round(np.exp(math.log(4096) + 0.8 * rng.standard_normal(batch))), 256, 32768)
+    return build(P.astype(np.int64), np.ones(batch, np.int64), 64, 8, 128, seed=seed, rng=rng,
+                 name="decode_70b")
+
+
 # --------------------------------------------------------------------------- structured suites
 # Each modifies the logical arrays and rebuilds the pool; none computes attention.
 
