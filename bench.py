@@ -199,6 +199,10 @@ def main():
     t_att = float(np.mean(att)) * 1e-3
 
     achieved = F / t_att / 1e12
+    g = w.num_q_heads // w.num_kv_heads
+    small = g <= 16 and int(w.new_lens.max()) * g <= 16  # the library's automatic tiling rule
+    kernel_name = (("attention_small_kernel" if small else "attention_kernel") + f"<{D}>"
+                   + " (+ split merge when the plan splits)")
     # the binding roof follows the workload's arithmetic intensity (flop per algorithmic byte)
     ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
     hbm_bound = F / w.attn_bytes() < ridge
@@ -232,7 +236,7 @@ def main():
         "algorithmic": {"flops": F, "attn_bytes": w.attn_bytes(), "append_bytes": w.append_bytes()},
         "roofline": {**roof,
                      "traffic": profiled_traffic(w.name),
-                     "kernel": "attention_kernel<128> (+ split merge when the plan splits)",
+                     "kernel": kernel_name,
                      "arithmetic_intensity": F / w.attn_bytes(),
                      "mfma_frac": achieved / PEAK_BF16_TFLOPS,
                      "hbm_gbs_algorithmic": w.attn_bytes() / t_att / 1e9},

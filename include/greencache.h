@@ -39,9 +39,9 @@
  *   - Errors detectable on the host are returned before anything is enqueued
  *     and leave every buffer untouched. A block id outside [0, num_blocks) in
  *     a table entry the batch needs is not checked on the host: the kernels
- *     skip such pages (append writes nothing there; attention reads zeros),
- *     so a bad id never causes an out-of-bounds access, but the result is
- *     then undefined. Two requests appending into the same slot race.
+ *     never access memory through such an id (append writes nothing there;
+ *     attention skips the page or reads block 0 in its place), so a bad id
+ *     never causes an out-of-bounds access, but the result is then undefined. Two requests appending into the same slot race.
  *     GC_ERR_HIP reports a failed launch; the HIP error is not cleared.
  *   - batch == 0 or T == 0: GC_OK, nothing is enqueued.
  */
@@ -61,7 +61,8 @@ typedef enum gc_status {
     GC_OK = 0,
     GC_ERR_NULL_ARG = -1,    /* a required pointer is NULL */
     GC_ERR_BAD_SHAPE = -2,   /* negative length, Hq % Hkv != 0, non-positive sizes, bad scale */
-    GC_ERR_UNSUPPORTED = -3, /* head_dim not 64/128, page_size != 16, Hq/Hkv > 128, Hkv > 65535 */
+    GC_ERR_UNSUPPORTED = -3, /* head_dim not 64/128, page_size != 16, Hq/Hkv > 128, Hkv > 65535,
+                                small tiles forced with Hq/Hkv > 16 */
     GC_ERR_BLOCK_TABLE = -4, /* ceil((P_r + n_r) / page_size) > max_blocks_per_seq */
     GC_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required */
     GC_ERR_HIP = -6          /* a HIP launch or runtime call failed */
@@ -89,12 +90,23 @@ typedef struct gc_batch {
     const int32_t* block_tables_dev; /* [B][max_blocks_per_seq] device, physical block ids */
 } gc_batch;
 
-/* Work-split options of the attention call. Pass NULL for the defaults. */
+/* Tilings of the attention call (gc_plan_options.tiling). */
+typedef enum gc_tiling {
+    GC_TILES_AUTO = 0,    /* small tiles when every request has n_r * Hq / Hkv <= 16
+                             (decode-like batches), prefill tiles otherwise */
+    GC_TILES_PREFILL = 1, /* 128 query rows x 64 keys per tile, staged through LDS */
+    GC_TILES_SMALL = 2    /* 16 query rows x 32 keys per wavefront, read straight from
+                             global memory; needs Hq / Hkv <= 16 */
+} gc_tiling;
+
+/* Work-split and tiling options of the attention call. Pass NULL for the defaults. */
 typedef struct gc_plan_options {
     /* 0: automatic. > 0: split the keys of every query tile into chunks of this
-     * many 64-key tiles, merged by log-sum-exp. < 0: never split. */
+     * many key tiles (64 keys with prefill tiles, 32 with small tiles), merged
+     * by log-sum-exp. < 0: never split. */
     int32_t kv_split_tiles;
-    int32_t reserved[7];     /* must be zero */
+    int32_t tiling;          /* a gc_tiling value; other values: GC_ERR_BAD_SHAPE */
+    int32_t reserved[6];     /* must be zero */
 } gc_plan_options;
 
 /*

@@ -54,7 +54,12 @@ class BatchDesc(ctypes.Structure):
 
 
 class PlanOptions(ctypes.Structure):
-    _fields_ = [("kv_split_tiles", ctypes.c_int32), ("reserved", ctypes.c_int32 * 7)]
+    _fields_ = [("kv_split_tiles", ctypes.c_int32), ("tiling", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 6)]
+
+
+# gc_tiling values
+TILES_AUTO, TILES_PREFILL, TILES_SMALL = 0, 1, 2
 
 
 _lib = None
@@ -169,11 +174,12 @@ def _geo_from_pools(k_pool, v_pool, q_heads, batch: PagedBatch):
     return geometry(q_heads, Hkv, D, NB, batch.max_blocks_per_seq, S)
 
 
-def _opts(kv_split_tiles):
-    if kv_split_tiles is None:
+def _opts(kv_split_tiles, tiling=None):
+    if kv_split_tiles is None and tiling is None:
         return None
     o = PlanOptions()
-    o.kv_split_tiles = int(kv_split_tiles)
+    o.kv_split_tiles = int(kv_split_tiles or 0)
+    o.tiling = int(tiling or 0)
     return ctypes.byref(o)
 
 
@@ -193,19 +199,20 @@ def kv_append(k_new, v_new, k_pool, v_pool, batch: PagedBatch, stream=None):
     _check("gc_kv_append", st, lib)
 
 
-def workspace_size(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None) -> int:
+def workspace_size(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None,
+                   tiling=None) -> int:
     lib = load_library()
     geo = _geo_from_pools(k_pool, v_pool, num_q_heads, batch)
     out = ctypes.c_size_t(0)
     st = lib.gc_prefix_prefill_workspace_size(ctypes.byref(geo), ctypes.byref(batch.desc()),
-                                              _opts(kv_split_tiles), ctypes.byref(out))
+                                              _opts(kv_split_tiles, tiling), ctypes.byref(out))
     _check("gc_prefix_prefill_workspace_size", st, lib)
     return int(out.value)
 
 
-def alloc_workspace(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None):
+def alloc_workspace(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None, tiling=None):
     import torch
-    n = workspace_size(num_q_heads, k_pool, v_pool, batch, kv_split_tiles)
+    n = workspace_size(num_q_heads, k_pool, v_pool, batch, kv_split_tiles, tiling)
     return torch.empty(max(n, 256), dtype=torch.uint8, device=batch.device)
 
 
@@ -231,23 +238,24 @@ def _attn_args(q, k_pool, v_pool, batch, out, lse, workspace):
     return geo, out
 
 
-def plan(num_q_heads, k_pool, v_pool, batch: PagedBatch, workspace, kv_split_tiles=None, stream=None):
+def plan(num_q_heads, k_pool, v_pool, batch: PagedBatch, workspace, kv_split_tiles=None, stream=None,
+         tiling=None):
     import torch
     lib = load_library()
     _require(workspace, torch.uint8, "workspace", batch.device)
     geo = _geo_from_pools(k_pool, v_pool, num_q_heads, batch)
     st = lib.gc_prefix_prefill_plan(ctypes.byref(geo), ctypes.byref(batch.desc()),
-                                    _opts(kv_split_tiles), workspace.data_ptr(),
+                                    _opts(kv_split_tiles, tiling), workspace.data_ptr(),
                                     workspace.numel(), _stream_handle(stream))
     _check("gc_prefix_prefill_plan", st, lib)
 
 
 def run(q, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=None,
-        kv_split_tiles=None, stream=None):
+        kv_split_tiles=None, stream=None, tiling=None):
     lib = load_library()
     geo, out = _attn_args(q, k_pool, v_pool, batch, out, lse, workspace)
     st = lib.gc_prefix_prefill_run(ctypes.byref(geo), ctypes.byref(batch.desc()),
-                                   _opts(kv_split_tiles), q.data_ptr(), k_pool.data_ptr(),
+                                   _opts(kv_split_tiles, tiling), q.data_ptr(), k_pool.data_ptr(),
                                    v_pool.data_ptr(), float(scale), out.data_ptr(),
                                    lse.data_ptr() if lse is not None else None,
                                    workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
@@ -256,7 +264,7 @@ def run(q, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=No
 
 
 def prefix_prefill_attention(q, k_pool, v_pool, batch: PagedBatch, scale, workspace=None,
-                             out=None, lse=None, kv_split_tiles=None, stream=None):
+                             out=None, lse=None, kv_split_tiles=None, stream=None, tiling=None):
     """Attention of the new tokens (q: [T][Hq][D] bf16) over cached prefix + new keys.
 
     The pools must already hold the new tokens' K/V (call kv_append first).
@@ -264,10 +272,10 @@ def prefix_prefill_attention(q, k_pool, v_pool, batch: PagedBatch, scale, worksp
     """
     lib = load_library()
     if workspace is None:
-        workspace = alloc_workspace(q.shape[1], k_pool, v_pool, batch, kv_split_tiles)
+        workspace = alloc_workspace(q.shape[1], k_pool, v_pool, batch, kv_split_tiles, tiling)
     geo, out = _attn_args(q, k_pool, v_pool, batch, out, lse, workspace)
     st = lib.gc_prefix_prefill_attention(ctypes.byref(geo), ctypes.byref(batch.desc()),
-                                         _opts(kv_split_tiles), q.data_ptr(), k_pool.data_ptr(),
+                                         _opts(kv_split_tiles, tiling), q.data_ptr(), k_pool.data_ptr(),
                                          v_pool.data_ptr(), float(scale), out.data_ptr(),
                                          lse.data_ptr() if lse is not None else None,
                                          workspace.data_ptr(), workspace.numel(),

@@ -15,7 +15,10 @@ using gc::RequestCounts;
 struct Shape {
     int64_t total_tokens = 0;
     int group = 1;
-    int tq = 1;
+    bool small = false;          // small-tile (decode) path
+    int block_m = gc::kBlockM;   // query rows per tile
+    int block_n = gc::kBlockN;   // keys per tile
+    int tq = 1;                  // new tokens per query tile
 };
 
 struct Plan {
@@ -37,7 +40,7 @@ gc_status check_common(const gc_geometry* geo, const gc_batch* b, Shape* sh) {
     if (geo->head_dim != 64 && geo->head_dim != 128) return GC_ERR_UNSUPPORTED;
     if (geo->page_size != gc::kPage) return GC_ERR_UNSUPPORTED;
     sh->group = group;
-    sh->tq = gc::tokens_per_tile(group);
+    sh->tq = gc::tokens_per_tile(group, sh->block_m);
     sh->total_tokens = 0;
     if (b->batch == 0) return GC_OK;
     if (b->prefix_lens_host == nullptr || b->new_lens_host == nullptr) return GC_ERR_NULL_ARG;
@@ -66,8 +69,31 @@ gc_status check_common(const gc_geometry* geo, const gc_batch* b, Shape* sh) {
 
 gc_status check_options(const gc_plan_options* o) {
     if (o == nullptr) return GC_OK;
-    for (int i = 0; i < 7; ++i)
+    if (o->tiling != GC_TILES_AUTO && o->tiling != GC_TILES_PREFILL && o->tiling != GC_TILES_SMALL)
+        return GC_ERR_BAD_SHAPE;
+    for (int i = 0; i < 6; ++i)
         if (o->reserved[i] != 0) return GC_ERR_BAD_SHAPE;
+    return GC_OK;
+}
+
+// Tiling: small tiles (one wavefront per 16 query rows, keys read straight from
+// global memory) when every request's new tokens fit one such tile, which is the
+// decode case; the LDS-staged prefill tiles otherwise.
+gc_status choose_tiling(const gc_batch* b, const gc_plan_options* o, Shape* sh) {
+    const int want = o == nullptr ? GC_TILES_AUTO : o->tiling;
+    bool small = false;
+    if (want == GC_TILES_SMALL) {
+        if (sh->group > gc::kDecM) return GC_ERR_UNSUPPORTED;
+        small = true;
+    } else if (want == GC_TILES_AUTO && sh->group <= gc::kDecM) {
+        small = true;
+        for (int r = 0; r < b->batch && small; ++r)
+            small = (int64_t)b->new_lens_host[r] * sh->group <= gc::kDecM;
+    }
+    sh->small = small;
+    sh->block_m = small ? gc::kDecM : gc::kBlockM;
+    sh->block_n = small ? gc::kDecN : gc::kBlockN;
+    sh->tq = gc::tokens_per_tile(sh->group, sh->block_m);
     return GC_OK;
 }
 
@@ -91,9 +117,10 @@ int device_cus() {
     return cus;
 }
 
-// Split policy: keep whole query tiles when there are at least as many
-// workgroups as resident slots (two per compute unit); otherwise cut the keys
-// into chunks so that the launch fills those slots.
+// Split policy: keep whole query tiles when there are at least as many work
+// items as resident slots (two prefill workgroups per compute unit, or eight
+// small-tile wavefronts); otherwise cut the keys into chunks of at least 512
+// keys so that the launch fills those slots.
 int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
                  const gc_plan_options* o) {
     if (o != nullptr && o->kv_split_tiles != 0) return o->kv_split_tiles > 0 ? o->kv_split_tiles : 0;
@@ -103,15 +130,15 @@ int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
         for (int q0 = 0; q0 < n; q0 += sh.tq) {
             const int ntok = n - q0 < sh.tq ? n - q0 : sh.tq;
             units += 1;
-            tiles += gc::key_tiles(P, q0, ntok);
+            tiles += gc::key_tiles(P, q0, ntok, sh.block_n);
         }
     }
     units *= geo->num_kv_heads;
     tiles *= geo->num_kv_heads;
-    const int64_t target = 2LL * device_cus();
+    const int64_t target = (sh.small ? 8LL : 2LL) * device_cus();
     if (units >= target || units == 0) return 0;
     int64_t chunk = (tiles + target - 1) / target;
-    if (chunk < 8) chunk = 8;  // at least 512 keys per chunk
+    if (chunk < 512 / sh.block_n) chunk = 512 / sh.block_n;
     return chunk > INT32_MAX ? 0 : (int)chunk;
 }
 
@@ -120,14 +147,15 @@ gc_status make_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
     pl->chunk = choose_chunk(geo, b, sh, o);
     pl->items = pl->combines = pl->partials = 0;
     for (int r = 0; r < b->batch; ++r) {
-        const RequestCounts c = gc::request_counts(b->prefix_lens_host[r], b->new_lens_host[r], sh.tq, pl->chunk);
+        const RequestCounts c = gc::request_counts(b->prefix_lens_host[r], b->new_lens_host[r], sh.tq,
+                                                   pl->chunk, sh.block_n);
         pl->items += c.items;
         pl->combines += c.combines;
         pl->partials += c.partials;
     }
     if (pl->items > (int64_t)INT32_MAX / geo->num_kv_heads) return GC_ERR_BAD_SHAPE;
     pl->layout = gc::workspace_layout(b->batch, pl->items, pl->combines, pl->partials,
-                                      geo->num_kv_heads, geo->head_dim);
+                                      geo->num_kv_heads, geo->head_dim, sh.block_m);
     return GC_OK;
 }
 
@@ -141,6 +169,8 @@ gc_status plan_checked(const gc_geometry* geo, const gc_batch* b, const gc_plan_
     gc_status st = check_common(geo, b, sh);
     if (st != GC_OK) return st;
     st = check_options(o);
+    if (st != GC_OK) return st;
+    st = choose_tiling(b, o, sh);
     if (st != GC_OK) return st;
     if (sh->total_tokens == 0) return GC_OK;
     return make_plan(geo, b, *sh, o, pl);
@@ -162,6 +192,7 @@ gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& s
     a.batch = b->batch;
     a.tq = sh.tq;
     a.chunk = pl.chunk;
+    a.block_n = sh.block_n;
     a.expect_items = (int32_t)pl.items;
     a.expect_combines = (int32_t)pl.combines;
     a.expect_partials = (int32_t)pl.partials;
@@ -190,7 +221,9 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
     a.num_blocks = geo->num_blocks;
     a.max_blocks = geo->max_blocks_per_seq;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
-    if (gc::launch_attention(a, geo->head_dim, pl.items, stream) != hipSuccess) return GC_ERR_HIP;
+    const hipError_t e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, stream)
+                                  : gc::launch_attention(a, geo->head_dim, pl.items, stream);
+    if (e != hipSuccess) return GC_ERR_HIP;
     if (pl.combines > 0) {
         gc::CombineArgs c{};
         c.out = a.out;
@@ -206,6 +239,7 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
         c.tq = sh.tq;
         c.batch = b->batch;
         c.num_partials = (int32_t)pl.partials;
+        c.block_m = sh.block_m;
         if (gc::launch_combine(c, geo->head_dim, pl.combines, stream) != hipSuccess) return GC_ERR_HIP;
     }
     return GC_OK;
@@ -319,7 +353,7 @@ const char* gc_status_string(gc_status s) {
         case GC_OK: return "GC_OK: success";
         case GC_ERR_NULL_ARG: return "GC_ERR_NULL_ARG: a required pointer is NULL";
         case GC_ERR_BAD_SHAPE: return "GC_ERR_BAD_SHAPE: invalid size, length or scale";
-        case GC_ERR_UNSUPPORTED: return "GC_ERR_UNSUPPORTED: head_dim must be 64 or 128, page_size 16, Hq/Hkv <= 128";
+        case GC_ERR_UNSUPPORTED: return "GC_ERR_UNSUPPORTED: head_dim must be 64 or 128, page_size 16, Hq/Hkv <= 128 (<= 16 for small tiles)";
         case GC_ERR_BLOCK_TABLE: return "GC_ERR_BLOCK_TABLE: block table too short for a request";
         case GC_ERR_WORKSPACE: return "GC_ERR_WORKSPACE: workspace missing or too small";
         case GC_ERR_HIP: return "GC_ERR_HIP: a HIP launch failed";

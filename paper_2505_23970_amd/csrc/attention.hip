@@ -365,10 +365,10 @@ template <int D>
 __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineArgs a) {
     constexpr int CPR = D / 4;                      // float4 chunks per row
     constexpr int kRows = kCombineThreads / CPR;    // rows per workgroup
-    static_assert(kBlockM % kRows == 0, "row groups");
-    constexpr int kGroups = kBlockM / kRows;
-    const unsigned tile = blockIdx.x / kGroups;
-    const int m = (int)(blockIdx.x % kGroups) * kRows + (int)threadIdx.x / CPR;
+    const int groups = ceil_div(a.block_m, kRows);
+    const unsigned tile = blockIdx.x / (unsigned)groups;
+    const int m = (int)(blockIdx.x % (unsigned)groups) * kRows + (int)threadIdx.x / CPR;
+    if (m >= a.block_m) return;
     const int c4 = (int)threadIdx.x % CPR;
     const int kvh = (int)(tile % (unsigned)a.num_kv_heads);
     const CombineItem ci = a.combines[tile / (unsigned)a.num_kv_heads];
@@ -381,8 +381,8 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineA
     const int ntok = min(a.tq, n - ci.q0);
     const int t = m / a.group, hl = m - t * a.group;
     if (t >= ntok) return;
-    const int64_t row0 = ((int64_t)ci.part_base * a.num_kv_heads + kvh) * kBlockM + m;
-    const int64_t split_stride = (int64_t)a.num_kv_heads * kBlockM;  // rows between chunks
+    const int64_t row0 = ((int64_t)ci.part_base * a.num_kv_heads + kvh) * a.block_m + m;
+    const int64_t split_stride = (int64_t)a.num_kv_heads * a.block_m;  // rows between chunks
     float mx = -INFINITY;
     for (int s = 0; s < ci.ns; ++s) mx = fmaxf(mx, a.part_lse[row0 + s * split_stride]);
     float tot = 0.f;
@@ -415,7 +415,7 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, 
 }
 
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s) {
-    const int groups = kBlockM / (kCombineThreads / (head_dim / 4));
+    const int groups = ceil_div(a.block_m, kCombineThreads / (head_dim / 4));
     const dim3 grid((unsigned)(num_combines * a.num_kv_heads * groups));
     if (head_dim == 128)
         combine_kernel<128><<<grid, kCombineThreads, 0, s>>>(a);

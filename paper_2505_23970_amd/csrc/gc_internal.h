@@ -6,13 +6,18 @@
 
 namespace gc {
 
-// Attention tiling: a workgroup of 4 wavefronts owns 128 query rows
-// (query heads of one KV head stacked over consecutive new tokens) and walks
-// the request's keys in tiles of 64 (four 16-key pool pages).
+// Attention tiling, prefill path: a workgroup of 4 wavefronts owns 128 query
+// rows (query heads of one KV head stacked over consecutive new tokens) and
+// walks the request's keys in tiles of 64 (four 16-key pool pages).
 constexpr int kRowsPerWave = 32;
 constexpr int kWaves = 4;
 constexpr int kBlockM = kRowsPerWave * kWaves;  // 128
 constexpr int kBlockN = 64;
+// Small-tile (decode) path: one wavefront owns 16 query rows and walks the keys
+// in tiles of 32 (two pages), straight from global memory.
+constexpr int kDecM = 16;
+constexpr int kDecN = 32;
+constexpr int kDecWaves = 4;                    // independent wavefronts per workgroup
 constexpr int kPage = 16;
 constexpr int kAttnThreads = kWaves * 64;
 constexpr int kPlanThreads = 256;
@@ -39,12 +44,13 @@ struct CombineItem {
 // itself); both must agree exactly.
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// new tokens per query tile for a GQA group of g query heads per KV head
-__host__ __device__ inline int tokens_per_tile(int group) { return kBlockM / group; }
+// new tokens per query tile of block_m rows for a GQA group of g query heads per KV head
+__host__ __device__ inline int tokens_per_tile(int group, int block_m) { return block_m / group; }
 
-__host__ __device__ inline int key_tiles(int prefix, int q0, int ntok) {
-    return ceil_div(prefix + q0 + ntok, kBlockN);
+__host__ __device__ inline int key_tiles(int prefix, int q0, int ntok, int block_n) {
+    return ceil_div(prefix + q0 + ntok, block_n);
 }
 
 // number of key chunks of a query tile with kt key tiles; chunk <= 0 means never split
@@ -63,11 +69,11 @@ struct RequestCounts {
     int partials;  // partial slots (per KV head)
 };
 
-__host__ __device__ inline RequestCounts request_counts(int prefix, int n, int tq, int chunk) {
+__host__ __device__ inline RequestCounts request_counts(int prefix, int n, int tq, int chunk, int block_n) {
     RequestCounts c{0, 0, 0};
     for (int q0 = 0; q0 < n; q0 += tq) {
         int ntok = n - q0 < tq ? n - q0 : tq;
-        int ns = num_splits(key_tiles(prefix, q0, ntok), chunk);
+        int ns = num_splits(key_tiles(prefix, q0, ntok, block_n), chunk);
         c.items += ns;
         if (ns > 1) {
             c.combines += 1;
@@ -85,7 +91,7 @@ struct WorkspaceLayout {
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 inline WorkspaceLayout workspace_layout(int batch, int64_t items, int64_t combines,
-                                        int64_t partials, int num_kv_heads, int head_dim) {
+                                        int64_t partials, int num_kv_heads, int head_dim, int block_m) {
     WorkspaceLayout w{};
     size_t off = 0;
     w.status_off = off;
@@ -98,9 +104,9 @@ inline WorkspaceLayout workspace_layout(int batch, int64_t items, int64_t combin
     off = align_up(off + sizeof(int32_t) * 3 * (size_t)(batch + 1), 256);
     off = align_up(off + sizeof(WorkItem) * (size_t)(items > 0 ? items : 1), 256);
     w.part_lse_off = off;
-    off = align_up(off + sizeof(float) * (size_t)partials * num_kv_heads * kBlockM, 256);
+    off = align_up(off + sizeof(float) * (size_t)partials * num_kv_heads * block_m, 256);
     w.part_o_off = off;
-    off = align_up(off + sizeof(float) * (size_t)partials * num_kv_heads * kBlockM * head_dim, 256);
+    off = align_up(off + sizeof(float) * (size_t)partials * num_kv_heads * block_m * head_dim, 256);
     w.total = off;
     return w;
 }
@@ -125,7 +131,7 @@ struct PlanArgs {
     WorkItem* items;          // [items], sorted by cost, heaviest first
     CombineItem* combines;    // [combines]
     int32_t* status;          // status[0] = 0 when the device counts matched the host's
-    int32_t batch, tq, chunk;
+    int32_t batch, tq, chunk, block_n;
     int32_t expect_items, expect_combines, expect_partials;
 };
 
@@ -135,8 +141,8 @@ struct AttnArgs {
     const uint16_t* v_pool;
     uint16_t* out;
     float* lse;          // may be null
-    float* part_o;       // [partials][Hkv][128][D]
-    float* part_lse;     // [partials][Hkv][128]
+    float* part_o;       // [partials][Hkv][block_m][D]
+    float* part_lse;     // [partials][Hkv][block_m]
     const int32_t* prefix_lens;
     const int32_t* cu_new_lens;
     const int32_t* block_tables;
@@ -155,12 +161,13 @@ struct CombineArgs {
     const int32_t* cu_new_lens;
     const CombineItem* combines;
     int32_t num_q_heads, num_kv_heads, group, tq;
-    int32_t batch, num_partials;
+    int32_t batch, num_partials, block_m;
 };
 
 hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
+hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s);
 
 }  // namespace gc

@@ -72,7 +72,7 @@ __device__ __forceinline__ Tile tile_at(const PlanArgs& a, const Lens& l, int g)
     t.q0 = (g - l.cum[lo]) * a.tq;
     const int n = l.cu[lo + 1] - l.cu[lo];
     const int ntok = min(a.tq, n - t.q0);
-    t.kt = key_tiles(l.prefix[lo], t.q0, ntok);
+    t.kt = key_tiles(l.prefix[lo], t.q0, ntok, a.block_n);
     t.ns = num_splits(t.kt, a.chunk);
     return t;
 }

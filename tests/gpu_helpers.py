@@ -51,14 +51,14 @@ class DeviceRun:
         import paper_2505_23970_amd as gc
         gc.kv_append(self.k_new, self.v_new, self.k_pool, self.v_pool, self.batch)
 
-    def attention(self, kv_split_tiles=None, with_lse=True):
+    def attention(self, kv_split_tiles=None, with_lse=True, tiling=None):
         import torch
         import paper_2505_23970_amd as gc
         T, Hq, D = self.w.q.shape
         lse = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda") if with_lse else None
         out = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
         gc.prefix_prefill_attention(self.q, self.k_pool, self.v_pool, self.batch, self.w.scale,
-                                    out=out, lse=lse, kv_split_tiles=kv_split_tiles)
+                                    out=out, lse=lse, kv_split_tiles=kv_split_tiles, tiling=tiling)
         torch.cuda.synchronize()
         return out, lse
 

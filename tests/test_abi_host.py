@@ -106,6 +106,28 @@ def test_unsupported(lib):
     assert append_status(lib, geo(Hq=256, Hkv=1), b) == -3
 
 
+def test_tiling_option(lib):
+    b = HostBatch([40], [3])
+    bad = gc.PlanOptions(-1, 7)
+    assert run_status(lib, geo(), b, opts=bad) == -2                  # not a gc_tiling value
+    small = gc.PlanOptions(-1, gc.TILES_SMALL)
+    assert run_status(lib, geo(Hq=32, Hkv=1), b, opts=small) == -3    # 32 heads per KV head
+    # forced small tiles on 16 heads per KV head pass the host checks (a NULL pointer then fires)
+    nul = (None, 0x2000, 0x2000, 0x2000)
+    assert run_status(lib, geo(Hq=16, Hkv=1), b, opts=small, ptrs=nul) == -1
+    # the two tilings plan different work lists: 300 tokens at 4 heads per KV head
+    # are ten 128-row tiles or seventy-five 16-row tiles
+    b = HostBatch([40], [300])
+    sizes = {}
+    for t in (gc.TILES_PREFILL, gc.TILES_SMALL):
+        s = ctypes.c_size_t()
+        assert lib.gc_prefix_prefill_workspace_size(ctypes.byref(geo(maxb=30)), ctypes.byref(b.desc),
+                                                    ctypes.byref(gc.PlanOptions(-1, t)),
+                                                    ctypes.byref(s)) == 0
+        sizes[t] = s.value
+    assert sizes[gc.TILES_SMALL] > sizes[gc.TILES_PREFILL]
+
+
 def test_block_table_too_short(lib):
     assert append_status(lib, geo(maxb=2), HostBatch([20], [13])) == -4   # needs 3 pages
     # long enough: the next check (a NULL data pointer) is the one that fires,

@@ -31,16 +31,16 @@ def check_pool(run: H.DeviceRun, kp_ref, vp_ref):
     assert np.array_equal(vp, vp_ref), f"v_pool differs at {np.argwhere(vp != vp_ref)[:5]}"
 
 
-def full_check(w, kv_split_tiles=None, rows=None, contract=False):
+def full_check(w, kv_split_tiles=None, rows=None, contract=False, tiling=None):
     """Append + attention on the GPU vs. the oracle. `contract` adds the fixed
     max/mean absolute bounds, which are stated for the configs' value scale."""
     say(f"case {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
-        f"T={w.total_new} split={kv_split_tiles}")
+        f"T={w.total_new} split={kv_split_tiles} tiling={tiling}")
     kp_ref, vp_ref = H.oracle_pools(w)
     run = H.DeviceRun(w)
     run.append()
     check_pool(run, kp_ref, vp_ref)
-    out, lse = run.attention(kv_split_tiles=kv_split_tiles)
+    out, lse = run.attention(kv_split_tiles=kv_split_tiles, tiling=tiling)
     ref_out, ref_lse = H.oracle_rows(w, kp_ref, vp_ref, rows=rows)
     return H.compare_attention(w, out, lse, ref_out, ref_lse, rows=rows, contract=contract), run, out
 
@@ -62,6 +62,12 @@ def test_config_sampled_rows(k):
     say(f"config {k}: {len(rows)} rows {info}")
 
 
+def test_decode_workload_sampled():
+    w = W.decode_variant()
+    info, _, _ = full_check(w, rows=H.sample_rows(w, seed=50), contract=True)
+    say(f"decode, 32 requests: {info}")
+
+
 def test_short_suffix_variant_sampled():
     w = W.short_suffix_variant()
     info, _, _ = full_check(w, rows=H.sample_rows(w, seed=40), contract=True)
@@ -79,6 +85,16 @@ SUITE_SHAPE = dict(prefix_lens=[300, 1000, 33, 0], new_lens=[77, 20, 130, 45],
 def test_value_scales(values, split):
     w = W.build(seed=100, values=values, name=f"suite_{values}", **SUITE_SHAPE)
     full_check(w, kv_split_tiles=split)
+
+
+@pytest.mark.parametrize("values", ["unit", "peaked"])
+@pytest.mark.parametrize("split", [None, 3])
+def test_small_tiles_on_multi_token_requests(values, split):
+    """The small-tile path forced on requests with up to 130 new tokens: many
+    2-token query tiles per request, causal masking inside each."""
+    import paper_2505_23970_amd as gc
+    w = W.build(seed=101, values=values, name=f"small_{values}", **SUITE_SHAPE)
+    full_check(w, kv_split_tiles=split, tiling=gc.TILES_SMALL)
 
 
 @pytest.mark.parametrize("split", [None, 1])
@@ -165,10 +181,15 @@ EDGES = [
 
 @pytest.mark.parametrize("name,P,n,Hq,Hkv,D", EDGES, ids=[e[0] for e in EDGES])
 def test_edge_cases(name, P, n, Hq, Hkv, D):
+    import paper_2505_23970_amd as gc
     w = W.build(P, n, Hq, Hkv, D, seed=200 + EDGES.index((name, P, n, Hq, Hkv, D)),
                 values="unit", name=name)
     full_check(w)
     full_check(w, kv_split_tiles=1)
+    full_check(w, tiling=gc.TILES_PREFILL)
+    if Hq // Hkv <= 16:
+        full_check(w, tiling=gc.TILES_SMALL)
+        full_check(w, kv_split_tiles=1, tiling=gc.TILES_SMALL)
 
 
 def test_batch_beyond_lds_plan_limit():
