@@ -165,6 +165,16 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       void* workspace, size_t workspace_bytes,
                                       hipStream_t stream);
 
+/*
+ * Calibration, not part of the attention path: read every byte of `buf`
+ * (device memory, `bytes` a multiple of 16) once as a streaming reduction,
+ * writing GC_READ_PROBE_SINK_WORDS 32-bit words to `sink` (device). Timing it
+ * gives the sustained HBM read rate that the memory-bound attention cases are
+ * also reported against (the nominal 8 TB/s is not reached by a read stream).
+ */
+#define GC_READ_PROBE_SINK_WORDS (2048 * 256)
+gc_status gc_read_bandwidth_probe(const void* buf, size_t bytes, void* sink, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* gc_status_string(gc_status status);
 

@@ -23,7 +23,9 @@ STATUS_NAMES = {0: "GC_OK", -1: "GC_ERR_NULL_ARG", -2: "GC_ERR_BAD_SHAPE", -3: "
                 -4: "GC_ERR_BLOCK_TABLE", -5: "GC_ERR_WORKSPACE", -6: "GC_ERR_HIP"}
 
 EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefill_plan",
-            "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_status_string")
+            "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_read_bandwidth_probe",
+            "gc_status_string")
+READ_PROBE_SINK_WORDS = 2048 * 256
 
 
 class GcError(RuntimeError):
@@ -85,6 +87,8 @@ def load_library(path: str | None = None):
     for fn in (lib.gc_prefix_prefill_run, lib.gc_prefix_prefill_attention):
         fn.restype = i32
         fn.argtypes = [G, Bp, O, vp, vp, vp, ctypes.c_float, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gc_read_bandwidth_probe.restype = i32
+    lib.gc_read_bandwidth_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
     lib.gc_status_string.restype = ctypes.c_char_p
     lib.gc_status_string.argtypes = [i32]
     if path is None:
@@ -261,6 +265,21 @@ def run(q, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=No
                                    workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
     _check("gc_prefix_prefill_run", st, lib)
     return out
+
+
+def read_bandwidth_probe(buf, sink=None, stream=None):
+    """Enqueue one streaming read of every byte of `buf` (a device tensor whose size
+    is a multiple of 16 bytes); returns the sink tensor it writes."""
+    import torch
+    lib = load_library()
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    if sink is None:
+        sink = torch.empty(READ_PROBE_SINK_WORDS, dtype=torch.int32, device=buf.device)
+    st = lib.gc_read_bandwidth_probe(buf.data_ptr(), buf.numel() * buf.element_size(), sink.data_ptr(),
+                                     _stream_handle(stream))
+    _check("gc_read_bandwidth_probe", st, lib)
+    return sink
 
 
 def prefix_prefill_attention(q, k_pool, v_pool, batch: PagedBatch, scale, workspace=None,

@@ -118,9 +118,10 @@ int device_cus() {
 }
 
 // Split policy: keep whole query tiles when there are at least as many work
-// items as resident slots (two prefill workgroups per compute unit, or eight
-// small-tile wavefronts); otherwise cut the keys into chunks of at least 512
-// keys so that the launch fills those slots.
+// items as resident slots (two prefill workgroups per compute unit, or four
+// small-tile wavefronts); otherwise cut the keys into chunks (at least 512
+// keys, 1024 for small tiles, whose wavefronts each stream their own K/V) so
+// that the launch fills those slots.
 int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
                  const gc_plan_options* o) {
     if (o != nullptr && o->kv_split_tiles != 0) return o->kv_split_tiles > 0 ? o->kv_split_tiles : 0;
@@ -135,10 +136,11 @@ int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
     }
     units *= geo->num_kv_heads;
     tiles *= geo->num_kv_heads;
-    const int64_t target = (sh.small ? 8LL : 2LL) * device_cus();
+    const int64_t target = (sh.small ? 4LL : 2LL) * device_cus();
     if (units >= target || units == 0) return 0;
     int64_t chunk = (tiles + target - 1) / target;
-    if (chunk < 512 / sh.block_n) chunk = 512 / sh.block_n;
+    const int min_keys = sh.small ? 1024 : 512;
+    if (chunk < min_keys / sh.block_n) chunk = min_keys / sh.block_n;
     return chunk > INT32_MAX ? 0 : (int)chunk;
 }
 
@@ -345,6 +347,15 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
     st = enqueue_plan(geo, batch, sh, pl, workspace, stream);
     if (st != GC_OK) return st;
     return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream);
+}
+
+__attribute__((visibility("default")))
+gc_status gc_read_bandwidth_probe(const void* buf, size_t bytes, void* sink, hipStream_t stream) {
+    if (buf == nullptr || sink == nullptr) return GC_ERR_NULL_ARG;
+    if (bytes % 16 != 0) return GC_ERR_BAD_SHAPE;
+    if (bytes == 0) return GC_OK;
+    return gc::launch_read_probe(buf, bytes, static_cast<uint32_t*>(sink), stream) == hipSuccess ? GC_OK
+                                                                                               : GC_ERR_HIP;
 }
 
 __attribute__((visibility("default")))

@@ -356,8 +356,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
     }
 }
 
-// Merge the key chunks of one split query tile: lse = log sum_s exp(lse_s),
-// o = sum_s exp(lse_s - lse) o_s, in a fixed chunk order (deterministic).
+// Merge the key chunks of one split query tile: with m = max_s lse_s,
+// lse = m + log sum_s exp(lse_s - m) and o = sum_s exp(lse_s - m) o_s / sum_s exp(lse_s - m),
+// in a fixed chunk order (deterministic).
 // A workgroup merges kCombineRows rows of one (query tile, KV head); a thread
 // owns four consecutive output elements of one row, so the partial rows are
 // read with coalesced 16-byte loads.
@@ -383,18 +384,39 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineA
     if (t >= ntok) return;
     const int64_t row0 = ((int64_t)ci.part_base * a.num_kv_heads + kvh) * a.block_m + m;
     const int64_t split_stride = (int64_t)a.num_kv_heads * a.block_m;  // rows between chunks
+    // chunks are read kBatch at a time with independent loads (the merge is bound by
+    // memory latency, not arithmetic); the sums still run in chunk order
+    constexpr int kBatch = 8;
     float mx = -INFINITY;
-    for (int s = 0; s < ci.ns; ++s) mx = fmaxf(mx, a.part_lse[row0 + s * split_stride]);
-    float tot = 0.f;
-    for (int s = 0; s < ci.ns; ++s) tot += expf(a.part_lse[row0 + s * split_stride] - mx);
-    const float lse_tot = mx + logf(tot);
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ci.ns; ++s) {
-        const int64_t pr = row0 + s * split_stride;
-        const float w = expf(a.part_lse[pr] - lse_tot);
-        const f32x4 v = *reinterpret_cast<const f32x4*>(a.part_o + pr * D + 4 * c4);
-        acc += w * v;
+    for (int s0 = 0; s0 < ci.ns; s0 += kBatch) {
+        float l[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            l[u] = s0 + u < ci.ns ? a.part_lse[row0 + (s0 + u) * split_stride] : -INFINITY;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) mx = fmaxf(mx, l[u]);
     }
+    float tot = 0.f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < ci.ns; s0 += kBatch) {
+        float l[kBatch];
+        f32x4 v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const bool ok = s0 + u < ci.ns;
+            const int64_t pr = row0 + (int64_t)(ok ? s0 + u : s0) * split_stride;
+            l[u] = ok ? a.part_lse[pr] : -INFINITY;
+            v[u] = *reinterpret_cast<const f32x4*>(a.part_o + pr * D + 4 * c4);
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const float w = expf(l[u] - mx);  // 0 for the padding entries
+            tot += w;
+            acc += w * v[u];
+        }
+    }
+    const float lse_tot = mx + logf(tot);
+    acc *= 1.f / tot;
     const int64_t qrow = (int64_t)(cu + ci.q0 + t) * a.num_q_heads + kvh * a.group + hl;
     u32x2 w2;
     w2[0] = pack_bf16x2(acc[0], acc[1]);

@@ -8,13 +8,13 @@
 // tokens) and key tiles of 32 keys (two pool pages). Such work is bound by
 // reading K and V, so each wavefront owns one work item and reads its K and V
 // fragments straight from global memory into registers in the matrix-core
-// operand layouts (no LDS staging, no barriers), with the next tile's loads in
-// flight while the current tile is computed:
+// operand layouts (no LDS staging, no barriers), with the next two tiles' loads
+// in flight while the current tile is computed:
 //   S^T (32 keys x 16 rows)  = K . Q^T     two 16x16 blocks, MFMA 16x16x32 bf16
 //   O^T (D x 16 rows)       += V^T . P^T   D/16 blocks,     MFMA 16x16x32 bf16
-// The keys fed to score block b are permuted so that the score accumulators
-// are already laid out as the P^T operand: lane group g (lanes 16g..16g+15)
-// holds keys 8g..8g+7 of the tile for its row, in order.
+// Score block b covers page b of the tile; the k order of the PV product is
+// permuted to match, so the score accumulators are already laid out as the P^T
+// operand and every global load reads a single page.
 #include "gc_internal.h"
 
 namespace gc {
@@ -28,6 +28,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(4))) int32_t* scalar_i32p;
 
 constexpr float kLn2 = 0.69314718055994530942f;
+// Buffer resource word 3 for raw (untyped) loads: 32-bit data format.
+constexpr int kBufferFlags = 0x00020000;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     const bf16x2 p = {(__bf16)lo, (__bf16)hi};
@@ -49,7 +51,7 @@ __device__ __forceinline__ float row_sum4(float x) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kDecWaves * 64) void attention_small_kernel(const AttnArgs a, int64_t units) {
+__global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(const AttnArgs a, int64_t units) {
     constexpr int KS = D / 32;                    // k-steps of QK^T
     constexpr int DB = D / 16;                    // 16-row blocks of O^T
     constexpr int kTileLog2Thresh = 8;            // rescale only when the max grows by > 2^8
@@ -85,18 +87,23 @@ __global__ __launch_bounds__(kDecWaves * 64) void attention_small_kernel(const A
         qf[s] = row_ok ? *reinterpret_cast<const bf16x8*>(a.q + qrow * D + 32 * s + 8 * g4)
                        : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
 
-    // K rows fed to score block b at operand row i = j: key 8 (i >> 2) + 4 b + (i & 3)
-    // of the tile, so accumulator value v of block b is key 8 g4 + 4 b + v.
-    const int krow[2] = {8 * (j >> 2) + (j & 3), 8 * (j >> 2) + 4 + (j & 3)};
+    // Score block b holds the 16 keys of page b of the tile (operand row i = key
+    // slot i), so accumulator value v of block b is key 16 b + 4 g4 + v. The P^T
+    // operand takes value (b, v) as its k index 8 g4 + 4 b + v; the V^T operand
+    // uses the same key order: lane (d, g4) holds slots 4 g4 .. 4 g4 + 3 of both
+    // pages. Every load reads one page, at a wave-uniform page address plus a
+    // per-lane offset.
     const scalar_i32p table = (scalar_i32p)(a.block_tables + (int64_t)r * a.max_blocks);
-    const int64_t page_elems = (int64_t)kPage * D;
-    const int64_t block_elems = (int64_t)a.num_kv_heads * page_elems;
-    const uint16_t* kbase = a.k_pool + (int64_t)kvh * page_elems;
-    const uint16_t* vbase = a.v_pool + (int64_t)kvh * page_elems;
+    const int64_t page_bytes = (int64_t)kPage * D * 2;
+    const int64_t block_bytes = (int64_t)a.num_kv_heads * page_bytes;
+    const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k_pool) + (int64_t)kvh * page_bytes;
+    const unsigned char* vbase = reinterpret_cast<const unsigned char*>(a.v_pool) + (int64_t)kvh * page_bytes;
+    const uint32_t k_off = (uint32_t)(j * D + 8 * g4) * 2;          // + 64 s bytes per k-step
+    const uint32_t v_off = (uint32_t)(j * kPage + 4 * g4) * 2;      // + 512 db bytes per value block
 
     struct Frags {
         bf16x8 k[2][KS];
-        bf16x8 v[DB];
+        u32x2 v[2][DB];   // [page][value block]: four bf16 values
     };
     // Block ids of the two pages of tile kt (scalar loads, fetched a tile ahead of
     // their use); pages past the sequence end or with an out-of-range id read
@@ -112,19 +119,25 @@ __global__ __launch_bounds__(kDecWaves * 64) void attention_small_kernel(const A
         const bool ok = (lp < a.max_blocks) & (lp * kPage < L) & (blk >= 0) & (blk < a.num_blocks);
         return ok ? blk : 0;
     };
+    // Loads go through buffer resources (one per page, in scalar registers) with
+    // loop-invariant per-lane offsets, so a tile's loads need no address registers
+    // that could collide with fragments still in flight. A page resource covers
+    // exactly the page; nothing outside it can be read.
     auto load = [&](int kt, const Ids& ids, Frags& f) {
-        const int64_t b0 = page_block(kt, 0, ids.b0), b1 = page_block(kt, 1, ids.b1);
+        const int64_t blk[2] = {page_block(kt, 0, ids.b0), page_block(kt, 1, ids.b1)};
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
-            const int key = krow[b];
-            const uint16_t* kp = kbase + (key < kPage ? b0 : b1) * block_elems + (key & (kPage - 1)) * D + 8 * g4;
+            const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(kbase + blk[b] * block_bytes), (short)0, (int)page_bytes, kBufferFlags);
+            const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(vbase + blk[b] * block_bytes), (short)0, (int)page_bytes, kBufferFlags);
 #pragma unroll
-            for (int s = 0; s < KS; ++s) f.k[b][s] = *reinterpret_cast<const bf16x8*>(kp + 32 * s);
+            for (int s = 0; s < KS; ++s)
+                f.k[b][s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(kr, (int)k_off + 64 * s, 0, 0));
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+                f.v[b][db] = __builtin_amdgcn_raw_buffer_load_b64(vr, (int)v_off + 512 * db, 0, 0);
         }
-        // V^T operand of value block db: lane holds v[d = 16 db + j][keys 8 g4 .. +7]
-        const uint16_t* vp = vbase + ((g4 >> 1) ? b1 : b0) * block_elems + j * kPage + 8 * (g4 & 1);
-#pragma unroll
-        for (int db = 0; db < DB; ++db) f.v[db] = *reinterpret_cast<const bf16x8*>(vp + db * 16 * kPage);
     };
 
     f32x4 o[DB];
@@ -144,25 +157,25 @@ __global__ __launch_bounds__(kDecWaves * 64) void attention_small_kernel(const A
             for (int ks = 0; ks < KS; ++ks)
                 s[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[b][ks], qf[ks], s[b], 0, 0, 0);
         }
-        // s[b][v] is the score of tile key 8 g4 + 4 b + v
+        // s[b][v] is the score of tile key 16 b + 4 g4 + v
         const int key0 = kt * kDecN;
         if (key0 + kDecN - 1 > P + it.q0) {
-            const int rel = lim - key0 - 8 * g4;
+            const int rel = lim - key0 - 4 * g4;
 #pragma unroll
             for (int b = 0; b < 2; ++b)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) s[b][v] = (4 * b + v > rel) ? -INFINITY : s[b][v];
+                for (int v = 0; v < 4; ++v) s[b][v] = (16 * b + v > rel) ? -INFINITY : s[b][v];
             // values past the sequence end become 0 (weight 0 times a stale value)
-            const int bad = L - key0 - 8 * g4;  // first key of this lane's eight at or past the end
-            if (bad < 8) {
+            const int bad = L - key0 - 4 * g4;  // first of this lane's slots (16 b + v) at or past the end
+            if (bad < 20) {
 #pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    u32x4 w = __builtin_bit_cast(u32x4, f.v[db]);
+                for (int b = 0; b < 2; ++b)
 #pragma unroll
-                    for (int x = 0; x < 4; ++x)
-                        w[x] &= (2 * x < bad ? 0xFFFFu : 0u) | (2 * x + 1 < bad ? 0xFFFF0000u : 0u);
-                    f.v[db] = __builtin_bit_cast(bf16x8, w);
-                }
+                    for (int db = 0; db < DB; ++db)
+#pragma unroll
+                        for (int x = 0; x < 2; ++x)
+                            f.v[b][db][x] &= (16 * b + 2 * x < bad ? 0xFFFFu : 0u) |
+                                             (16 * b + 2 * x + 1 < bad ? 0xFFFF0000u : 0u);
             }
         }
         float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
@@ -189,26 +202,33 @@ __global__ __launch_bounds__(kDecWaves * 64) void attention_small_kernel(const A
         }
         const bf16x8 pf = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.v[db], pf, o[db], 0, 0, 0);
+        for (int db = 0; db < DB; ++db) {
+            const u32x4 vw = {f.v[0][db][0], f.v[0][db][1], f.v[1][db][0], f.v[1][db][1]};
+            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vw), pf, o[db], 0, 0, 0);
+        }
     };
 
-    // Two fragment sets used in turn (no register copies), and the next tile's loads
-    // issued unconditionally (the last tile loads itself again), so the compiler's
-    // wait before a tile's products covers exactly that tile's loads.
-    Frags fa, fb;
+    // Three fragment sets used in turn (no register copies): the loads of tiles kt+1
+    // and kt+2 are in flight while tile kt is computed. Loads are issued
+    // unconditionally (past the last tile the last tile is loaded again), so the
+    // compiler's wait before a tile's products covers exactly that tile's loads.
+    Frags f0, f1, f2;
     const int kt_end = it.kt_end, last = kt_end - 1;
     int kt = it.kt_begin;
-    load(kt, fetch_ids(kt), fa);
-    Ids ids = fetch_ids(min(kt + 1, last));
-    auto step = [&](Frags& cur, Frags& nxt) {
-        load(min(kt + 1, last), ids, nxt);
-        ids = fetch_ids(min(kt + 2, last));
+    load(kt, fetch_ids(kt), f0);
+    load(min(kt + 1, last), fetch_ids(min(kt + 1, last)), f1);
+    Ids ids = fetch_ids(min(kt + 2, last));
+    auto step = [&](Frags& cur, Frags& ahead2) {
+        load(min(kt + 2, last), ids, ahead2);
+        ids = fetch_ids(min(kt + 3, last));
         compute(kt, cur);
     };
     while (true) {
-        step(fa, fb);
+        step(f0, f2);
         if (++kt >= kt_end) break;
-        step(fb, fa);
+        step(f1, f0);
+        if (++kt >= kt_end) break;
+        step(f2, f1);
         if (++kt >= kt_end) break;
     }
 

@@ -26,6 +26,8 @@ constexpr int kAppendThreads = 256;
 constexpr int kCostBuckets = 2048;  // counting-sort buckets of the work list (cost in tiles)
 constexpr int kCombineThreads = 256;  // threads per split-merge workgroup
 constexpr int kPlanLdsBatch = 2048;   // batches up to this size are planned from LDS copies
+constexpr int kProbeBlocks = 2048;    // read-probe grid
+constexpr int kProbeThreads = 256;
 
 // One attention work item: query tile [q0, q0 + tq) of request r against key
 // tiles [kt_begin, kt_end). part >= 0 marks a split item whose normalised
@@ -168,6 +170,7 @@ hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
 hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
+hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s);
 
 }  // namespace gc

@@ -10,8 +10,8 @@
 //   2. a histogram of item costs (key tiles per item) in LDS, scanned so that
 //      the heaviest items come first;
 //   3. every item is written straight to its sorted position (an LDS cursor per
-//      cost bucket); split query tiles take their partial slots and merge entry
-//      from two LDS counters.
+//      cost bucket, advanced once per distinct chunk size of a tile); split query
+//      tiles take their partial slots and merge entry from two LDS counters.
 // The hardware dispatcher starts workgroups in index order, so the longest
 // items start first (longest-processing-time scheduling). Order inside a cost
 // bucket and slot numbers may differ between runs; results do not depend on
@@ -25,21 +25,29 @@
 namespace gc {
 namespace {
 
-// exclusive scan of one value per thread; *total receives the sum
+// exclusive scan of one value per thread; *total receives the sum (a scan inside
+// each wavefront, then one exchange of the wavefront totals through LDS)
 __device__ int block_exclusive_scan(int v, int* s_tmp, int* total) {
-    const int tid = threadIdx.x;
-    s_tmp[tid] = v;
-    __syncthreads();
-    for (int d = 1; d < kPlanThreads; d <<= 1) {
-        const int add = tid >= d ? s_tmp[tid - d] : 0;
-        __syncthreads();
-        s_tmp[tid] += add;
-        __syncthreads();
+    constexpr int kWavesPlan = kPlanThreads / 64;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(x, d);
+        if (lane >= d) x += y;
     }
-    const int incl = s_tmp[tid];
-    *total = s_tmp[kPlanThreads - 1];
+    if (lane == 63) s_tmp[wave] = x;
     __syncthreads();
-    return incl - v;
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPlan; ++w) {
+        const int t = s_tmp[w];
+        base += w < wave ? t : 0;
+        tot += t;
+    }
+    __syncthreads();  // s_tmp is reused by the next scan
+    *total = tot;
+    return base + x - v;
 }
 
 __device__ __forceinline__ int bucket_of(int cost) {
@@ -116,11 +124,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
     __threadfence_block();
     __syncthreads();
 
-    // 2. cost histogram
+    // 2. cost histogram. The ns chunks of a tile have kt / ns key tiles (rounded
+    // down) or one more, so two additions per tile cover all of its chunks.
     for (int g = tid; g < total_tiles; g += kPlanThreads) {
         const Tile t = tile_at(a, lens, g);
-        for (int s = 0; s < t.ns; ++s)
-            atomicAdd(&s_hist[bucket_of(split_begin(s + 1, t.kt, t.ns) - split_begin(s, t.kt, t.ns))], 1);
+        const int lo = t.kt / t.ns, n_hi = t.kt - lo * t.ns, n_lo = t.ns - n_hi;
+        if (n_lo > 0) atomicAdd(&s_hist[bucket_of(lo)], n_lo);
+        if (n_hi > 0) atomicAdd(&s_hist[bucket_of(lo + 1)], n_hi);
     }
     __syncthreads();
     constexpr int kPer = kCostBuckets / kPlanThreads;
@@ -157,9 +167,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
                 a.combines[ci] = CombineItem{t.r, t.q0, part0, t.ns};
             }
         }
+        // reserve the tile's positions in both cost buckets at once, then hand them out
+        const int lo = t.kt / t.ns, n_hi = t.kt - lo * t.ns, n_lo = t.ns - n_hi;
+        int pos_lo = n_lo > 0 ? atomicAdd(&s_hist[bucket_of(lo)], n_lo) : 0;
+        int pos_hi = n_hi > 0 ? atomicAdd(&s_hist[bucket_of(lo + 1)], n_hi) : 0;
         for (int s = 0; s < t.ns; ++s) {
             const int b0 = split_begin(s, t.kt, t.ns), b1 = split_begin(s + 1, t.kt, t.ns);
-            const int pos = atomicAdd(&s_hist[bucket_of(b1 - b0)], 1);
+            const int pos = b1 - b0 == lo ? pos_lo++ : pos_hi++;
             a.items[pos] = part0 == -2 ? WorkItem{-1, 0, 0, 0, -1, 0, 0, 0}
                                        : WorkItem{t.r, t.q0, b0, b1, part0 < 0 ? -1 : part0 + s, 0, 0, 0};
         }

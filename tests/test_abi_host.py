@@ -33,6 +33,13 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, name), name
 
 
+def test_read_probe_rejects_bad_arguments(lib):
+    assert lib.gc_read_bandwidth_probe(None, 1024, 0x2000, None) == -1
+    assert lib.gc_read_bandwidth_probe(0x2000, 1024, None, None) == -1
+    assert lib.gc_read_bandwidth_probe(0x2000, 1000, 0x2000, None) == -2   # not a multiple of 16
+    assert lib.gc_read_bandwidth_probe(0x2000, 0, 0x2000, None) == 0       # nothing to read, nothing enqueued
+
+
 def test_status_strings(lib):
     for code, name in gc.STATUS_NAMES.items():
         assert lib.gc_status_string(code).decode().startswith(name)

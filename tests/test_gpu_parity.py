@@ -297,3 +297,16 @@ def test_append_leaves_other_slots_alone_with_bad_block_ids():
     keep[skipped] = False
     assert np.array_equal(kp[keep], kp_ref[keep]) and np.array_equal(vp[keep], vp_ref[keep])
     assert np.array_equal(kp[skipped], w.k_pool[skipped])   # untouched
+
+
+def test_read_probe_reads_every_word():
+    """The calibration probe XOR-reduces each thread's 16-byte words: a buffer with one
+    non-zero word leaves exactly that word's bits in one sink entry."""
+    import torch
+    import paper_2505_23970_amd as gc
+    buf = torch.zeros(1 << 20, dtype=torch.int32, device="cuda")
+    buf[12345] = 0x5A5A
+    sink = gc.read_bandwidth_probe(buf)
+    torch.cuda.synchronize()
+    nz = torch.nonzero(sink).flatten().tolist()
+    assert len(nz) == 1 and int(sink[nz[0]].item()) == 0x5A5A
