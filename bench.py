@@ -106,10 +106,10 @@ def measured_read_gbs(mib=4096, reps=5):
 
 def profiled_traffic(workload):
     """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary of this workload, if it was taken on the current kernel source; else None."""
+    summary of this workload, if it was taken on the current source of the profiled
+    kernel; else None."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"attention_{workload}.md")
-    src = os.path.join(ROOT, "paper_2505_23970_amd", "csrc", "attention.hip")
     if not os.path.exists(path):
         return None
     rec = None
@@ -118,6 +118,9 @@ def profiled_traffic(workload):
             if line.startswith("traffic-json:"):
                 rec = json.loads(line.split(":", 1)[1])
     if rec is None:
+        return None
+    src = os.path.join(ROOT, rec.get("kernel_source", "paper_2505_23970_amd/csrc/attention.hip"))
+    if not os.path.exists(src):
         return None
     with open(src, "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()[:16]
