@@ -93,10 +93,13 @@ typedef struct gc_batch {
 /* Tilings of the attention call (gc_plan_options.tiling). */
 typedef enum gc_tiling {
     GC_TILES_AUTO = 0,    /* small tiles when every request has n_r * Hq / Hkv <= 16
-                             (decode-like batches), prefill tiles otherwise */
+                             (decode-like batches); otherwise wide or prefill tiles,
+                             by the amount of work (see gc_prefix_prefill_plan) */
     GC_TILES_PREFILL = 1, /* 128 query rows x 64 keys per tile, staged through LDS */
-    GC_TILES_SMALL = 2    /* 16 query rows x 32 keys per wavefront, read straight from
+    GC_TILES_SMALL = 2,   /* 16 query rows x 32 keys per wavefront, read straight from
                              global memory; needs Hq / Hkv <= 16 */
+    GC_TILES_WIDE = 3     /* 256 query rows x 64 keys per workgroup of 8 wavefronts,
+                             staged through LDS (twice the rows per copied K/V tile) */
 } gc_tiling;
 
 /* Work-split and tiling options of the attention call. Pass NULL for the defaults. */

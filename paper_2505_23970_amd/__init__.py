@@ -61,7 +61,7 @@ class PlanOptions(ctypes.Structure):
 
 
 # gc_tiling values
-TILES_AUTO, TILES_PREFILL, TILES_SMALL = 0, 1, 2
+TILES_AUTO, TILES_PREFILL, TILES_SMALL, TILES_WIDE = 0, 1, 2, 3
 
 
 _lib = None

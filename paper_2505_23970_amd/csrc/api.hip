@@ -12,10 +12,12 @@ namespace {
 
 using gc::RequestCounts;
 
+
 struct Shape {
     int64_t total_tokens = 0;
     int group = 1;
     bool small = false;          // small-tile (decode) path
+    bool wide = false;           // 8-wavefront prefill tiles
     int block_m = gc::kBlockM;   // query rows per tile
     int block_n = gc::kBlockN;   // keys per tile
     int tq = 1;                  // new tokens per query tile
@@ -69,7 +71,8 @@ gc_status check_common(const gc_geometry* geo, const gc_batch* b, Shape* sh) {
 
 gc_status check_options(const gc_plan_options* o) {
     if (o == nullptr) return GC_OK;
-    if (o->tiling != GC_TILES_AUTO && o->tiling != GC_TILES_PREFILL && o->tiling != GC_TILES_SMALL)
+    if (o->tiling != GC_TILES_AUTO && o->tiling != GC_TILES_PREFILL && o->tiling != GC_TILES_SMALL &&
+        o->tiling != GC_TILES_WIDE)
         return GC_ERR_BAD_SHAPE;
     for (int i = 0; i < 6; ++i)
         if (o->reserved[i] != 0) return GC_ERR_BAD_SHAPE;
@@ -78,20 +81,42 @@ gc_status check_options(const gc_plan_options* o) {
 
 // Tiling: small tiles (one wavefront per 16 query rows, keys read straight from
 // global memory) when every request's new tokens fit one such tile, which is the
-// decode case; the LDS-staged prefill tiles otherwise.
-gc_status choose_tiling(const gc_batch* b, const gc_plan_options* o, Shape* sh) {
+// decode case. Otherwise LDS-staged prefill tiles: wide ones (256 rows, 8
+// wavefronts, one workgroup per CU) when they would be at least 85 % full and
+// their count is not between one and two per CU (whole units there would leave
+// the last round of workgroups mostly idle, and below one per CU the keys are
+// split into equal chunks); 128-row tiles otherwise.
+int device_cus();
+
+gc_status choose_tiling(const gc_batch* b, const gc_plan_options* o, int num_kv_heads, Shape* sh) {
     const int want = o == nullptr ? GC_TILES_AUTO : o->tiling;
-    bool small = false;
+    bool small = false, wide = false;
     if (want == GC_TILES_SMALL) {
         if (sh->group > gc::kDecM) return GC_ERR_UNSUPPORTED;
         small = true;
-    } else if (want == GC_TILES_AUTO && sh->group <= gc::kDecM) {
-        small = true;
-        for (int r = 0; r < b->batch && small; ++r)
-            small = (int64_t)b->new_lens_host[r] * sh->group <= gc::kDecM;
+    } else if (want == GC_TILES_WIDE) {
+        wide = true;
+    } else if (want == GC_TILES_AUTO) {
+        if (sh->group <= gc::kDecM) {
+            small = true;
+            for (int r = 0; r < b->batch && small; ++r)
+                small = (int64_t)b->new_lens_host[r] * sh->group <= gc::kDecM;
+        }
+        if (!small) {
+            const int tq = gc::tokens_per_tile(sh->group, gc::kWideM);
+            int64_t units = 0, rows = 0;
+            for (int r = 0; r < b->batch; ++r) {
+                units += (b->new_lens_host[r] + tq - 1) / tq;
+                rows += (int64_t)b->new_lens_host[r] * sh->group;
+            }
+            const int64_t cus = device_cus();
+            const int64_t grid = units * num_kv_heads;
+            wide = rows * 100 >= units * gc::kWideM * 85 && !(grid > cus && grid < 2 * cus);
+        }
     }
     sh->small = small;
-    sh->block_m = small ? gc::kDecM : gc::kBlockM;
+    sh->wide = wide;
+    sh->block_m = small ? gc::kDecM : (wide ? gc::kWideM : gc::kBlockM);
     sh->block_n = small ? gc::kDecN : gc::kBlockN;
     sh->tq = gc::tokens_per_tile(sh->group, sh->block_m);
     return GC_OK;
@@ -118,10 +143,10 @@ int device_cus() {
 }
 
 // Split policy: keep whole query tiles when there are at least as many work
-// items as resident slots (two prefill workgroups per compute unit, or four
-// small-tile wavefronts); otherwise cut the keys into chunks (at least 512
-// keys, 1024 for small tiles, whose wavefronts each stream their own K/V) so
-// that the launch fills those slots.
+// items as resident slots (per compute unit: two 128-row workgroups, one wide
+// workgroup, or four small-tile wavefronts); otherwise cut the keys into chunks
+// (at least 512 keys, 1024 for small tiles, whose wavefronts each stream their
+// own K/V) so that the launch fills those slots.
 int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
                  const gc_plan_options* o) {
     if (o != nullptr && o->kv_split_tiles != 0) return o->kv_split_tiles > 0 ? o->kv_split_tiles : 0;
@@ -136,7 +161,7 @@ int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
     }
     units *= geo->num_kv_heads;
     tiles *= geo->num_kv_heads;
-    const int64_t target = (sh.small ? 4LL : 2LL) * device_cus();
+    const int64_t target = (sh.small ? 4LL : (sh.wide ? 1LL : 2LL)) * device_cus();
     if (units >= target || units == 0) return 0;
     int64_t chunk = (tiles + target - 1) / target;
     const int min_keys = sh.small ? 1024 : 512;
@@ -172,7 +197,7 @@ gc_status plan_checked(const gc_geometry* geo, const gc_batch* b, const gc_plan_
     if (st != GC_OK) return st;
     st = check_options(o);
     if (st != GC_OK) return st;
-    st = choose_tiling(b, o, sh);
+    st = choose_tiling(b, o, geo->num_kv_heads, sh);
     if (st != GC_OK) return st;
     if (sh->total_tokens == 0) return GC_OK;
     return make_plan(geo, b, *sh, o, pl);
@@ -224,7 +249,7 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
     a.max_blocks = geo->max_blocks_per_seq;
     a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
     const hipError_t e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, stream)
-                                  : gc::launch_attention(a, geo->head_dim, pl.items, stream);
+                                  : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, stream);
     if (e != hipSuccess) return GC_ERR_HIP;
     if (pl.combines > 0) {
         gc::CombineArgs c{};

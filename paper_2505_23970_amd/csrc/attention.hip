@@ -6,10 +6,10 @@
 // cached and new KV processed together; §2.1 prefill). Keys are gathered from
 // the paged pool through the block table.
 //
-// Work decomposition. A workgroup (4 wavefronts) owns one work item: 128 query
-// rows = the g query heads of one KV head stacked over 128/g consecutive new
-// tokens of one request, against a range of 64-key tiles. Each wavefront owns
-// 32 of the rows. Per key tile:
+// Work decomposition. A workgroup (4 wavefronts, or 8 for the wide tiling) owns
+// one work item: 128 (256) query rows = the g query heads of one KV head stacked
+// over consecutive new tokens of one request, against a range of 64-key tiles.
+// Each wavefront owns 32 of the rows. Per key tile:
 //   S^T (64 keys x 32 rows)  = K_tile . Q^T        two 32x32 blocks, MFMA 32x32x16 bf16
 //   online softmax on S^T in registers               fp32, base-2 exponent
 //   O^T (D x 32 rows)       += V_tile^T . P^T       D/32 blocks, MFMA 32x32x16 bf16
@@ -78,14 +78,15 @@ __device__ __forceinline__ void wait_vmem() {
     asm volatile("" ::: "memory");  // no LDS access moves above the wait
 }
 
-template <int D>
-__global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnArgs a) {
+template <int D, int WAVES>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const AttnArgs a) {
+    constexpr int kBlockRows = WAVES * kRowsPerWave;  // query rows of a work item
     constexpr int DK = D / 16;                      // k-steps of QK^T
     constexpr int DB = D / 32;                      // 32-row blocks of O^T
     constexpr int kPageBytes = kPage * D * 2;       // one (block, KV head) page of K or V
     constexpr int kTileBytes = kBlockN * D * 2;     // four pages
     constexpr int kKbPerPage = kPageBytes / 1024;   // 1 KiB pieces per page
-    constexpr int NI = kTileBytes / (kWaves * 1024);  // direct loads per wave per tensor per tile
+    constexpr int NI = kTileBytes / (WAVES * 1024);  // direct loads per wave per tensor per tile
     constexpr int kTileLog2Thresh = 8;              // rescale only when the max grows by > 2^8
 
     // K tile: [64 keys][D], row-major, 16-byte chunks XOR-swizzled by row.
@@ -135,8 +136,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
     // Direct global->LDS loads: instruction e of a wave moves 1 KiB piece 4e + wave of
     // a tile tensor, i.e. piece `sub` of page `page_of(e)`; lane i lands at byte 16 i.
     const int sub = wave % kKbPerPage;
-    static_assert(kWaves % kKbPerPage == 0, "piece layout");
-    auto page_of = [&](int e) -> int { return (kWaves * e + wave) / kKbPerPage; };
+    static_assert(WAVES % kKbPerPage == 0, "piece layout");
+    auto page_of = [&](int e) -> int { return (WAVES / kKbPerPage) * e + (wave & (WAVES - 1)) / kKbPerPage; };
     const int k_row = sub * (1024 / (2 * D)) + lane / (D / 8);         // key slot in the page
     const uint32_t k_src = k_row * (2 * D) + swz_k<D>(lane % (D / 8), k_row) * 16;
     const int v_d = sub * 32 + (lane >> 1);                            // value row (d) in the page
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(const AttnAr
             if (a.lse != nullptr && hh == 0) a.lse[qrow] = lse_v;
         }
     } else {
-        const int64_t prow_g = ((int64_t)it.part * a.num_kv_heads + kvh) * kBlockM + m;
+        const int64_t prow_g = ((int64_t)it.part * a.num_kv_heads + kvh) * kBlockRows + m;
         float* po = a.part_o + prow_g * D;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
@@ -427,12 +428,19 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineA
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s) {
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, hipStream_t s) {
     const dim3 grid((unsigned)(num_items * a.num_kv_heads));
-    if (head_dim == 128)
-        attention_kernel<128><<<grid, kAttnThreads, 0, s>>>(a);
-    else
-        attention_kernel<64><<<grid, kAttnThreads, 0, s>>>(a);
+    if (wide) {
+        if (head_dim == 128)
+            attention_kernel<128, kWideWaves><<<grid, kWideWaves * 64, 0, s>>>(a);
+        else
+            attention_kernel<64, kWideWaves><<<grid, kWideWaves * 64, 0, s>>>(a);
+    } else {
+        if (head_dim == 128)
+            attention_kernel<128, kWaves><<<grid, kWaves * 64, 0, s>>>(a);
+        else
+            attention_kernel<64, kWaves><<<grid, kWaves * 64, 0, s>>>(a);
+    }
     return hipGetLastError();
 }
 

@@ -20,6 +20,10 @@ constexpr int kDecN = 32;
 constexpr int kDecWaves = 4;                    // independent wavefronts per workgroup
 constexpr int kPage = 16;
 constexpr int kAttnThreads = kWaves * 64;
+// Wide prefill tiles: 8 wavefronts, 256 query rows per work item (one workgroup
+// per CU; every K/V tile copied into LDS feeds twice the rows).
+constexpr int kWideWaves = 8;
+constexpr int kWideM = kRowsPerWave * kWideWaves;  // 256
 constexpr int kPlanThreads = 256;
 constexpr int kAppendTokens = 16;  // new tokens per append workgroup
 constexpr int kAppendThreads = 256;
@@ -168,7 +172,7 @@ struct CombineArgs {
 
 hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, hipStream_t s);
 hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
 hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s);

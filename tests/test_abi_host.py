@@ -126,13 +126,13 @@ def test_tiling_option(lib):
     # are ten 128-row tiles or seventy-five 16-row tiles
     b = HostBatch([40], [300])
     sizes = {}
-    for t in (gc.TILES_PREFILL, gc.TILES_SMALL):
+    for t in (gc.TILES_PREFILL, gc.TILES_SMALL, gc.TILES_WIDE):
         s = ctypes.c_size_t()
         assert lib.gc_prefix_prefill_workspace_size(ctypes.byref(geo(maxb=30)), ctypes.byref(b.desc),
                                                     ctypes.byref(gc.PlanOptions(-1, t)),
                                                     ctypes.byref(s)) == 0
         sizes[t] = s.value
-    assert sizes[gc.TILES_SMALL] > sizes[gc.TILES_PREFILL]
+    assert sizes[gc.TILES_SMALL] > sizes[gc.TILES_PREFILL] >= sizes[gc.TILES_WIDE]
 
 
 def test_block_table_too_short(lib):

@@ -88,6 +88,15 @@ def test_value_scales(values, split):
 
 
 @pytest.mark.parametrize("values", ["unit", "peaked"])
+@pytest.mark.parametrize("split", [None, 2])
+def test_wide_tiles(values, split):
+    """256-row work items (8 wavefronts per workgroup) on the supplementary suite."""
+    import paper_2505_23970_amd as gc
+    w = W.build(seed=102, values=values, name=f"wide_{values}", **SUITE_SHAPE)
+    full_check(w, kv_split_tiles=split, tiling=gc.TILES_WIDE)
+
+
+@pytest.mark.parametrize("values", ["unit", "peaked"])
 @pytest.mark.parametrize("split", [None, 3])
 def test_small_tiles_on_multi_token_requests(values, split):
     """The small-tile path forced on requests with up to 130 new tokens: many
@@ -187,6 +196,8 @@ def test_edge_cases(name, P, n, Hq, Hkv, D):
     full_check(w)
     full_check(w, kv_split_tiles=1)
     full_check(w, tiling=gc.TILES_PREFILL)
+    full_check(w, tiling=gc.TILES_WIDE)
+    full_check(w, kv_split_tiles=1, tiling=gc.TILES_WIDE)
     if Hq // Hkv <= 16:
         full_check(w, tiling=gc.TILES_SMALL)
         full_check(w, kv_split_tiles=1, tiling=gc.TILES_SMALL)
