@@ -60,8 +60,11 @@ def _decode():
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    # The GPU raises its clocks over the first ~40 ms of sustained work after idling
+    # (the 70B chat attention runs at 520 us per call cold and 355 us warm), so the
+    # default warm-up is long enough to time the steady state of a serving loop.
+    ap.add_argument("--warmup", type=int, default=400)
     ap.add_argument("--workload", default="llama3_8b", choices=sorted(WORKLOADS))
     ap.add_argument("--kv-split-tiles", type=int, default=None,
                     help="override the automatic split policy (0 auto, <0 never, >0 tiles)")
