@@ -118,10 +118,14 @@ typedef struct gc_plan_options {
  * head h, the head_dim values of k_new[cu_r + i][h] and v_new[cu_r + i][h] are
  * copied bit for bit to slot (P_r + i) % page_size of block
  * block_tables[r][(P_r + i) / page_size]. No other pool byte changes.
- *   k_new, v_new : device bf16 [T][Hkv][D]
+ *   k_new, v_new : bf16 [T][Hkv][D], device memory or pinned host memory
+ *                  (hipHostMalloc), which the kernel reads directly over PCIe
  *   k_pool, v_pool: device bf16 pools (layout above), updated in place
  * Call it before the attention call, which reads the new tokens' K/V from the
- * pool.
+ * pool. The same call restores a cached prefix loaded back from the cache's
+ * host tier (§2.2: on a hit the stored KV is brought back before the new
+ * tokens are processed): pass prefix_lens = 0 and new_lens = the cached
+ * lengths, with k_new / v_new pointing at the cached K/V in pinned host memory.
  */
 gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch,
                        const void* k_new, const void* v_new,

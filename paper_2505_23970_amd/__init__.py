@@ -130,6 +130,7 @@ class PagedBatch:
 
     def __init__(self, prefix_lens, new_lens, block_tables, device="cuda"):
         import torch
+        self._restore = None
         self.prefix_lens = np.ascontiguousarray(prefix_lens, dtype=np.int32)
         self.new_lens = np.ascontiguousarray(new_lens, dtype=np.int32)
         bt = np.ascontiguousarray(block_tables, dtype=np.int32)
@@ -201,6 +202,36 @@ def kv_append(k_new, v_new, k_pool, v_pool, batch: PagedBatch, stream=None):
                           v_new.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(),
                           _stream_handle(stream))
     _check("gc_kv_append", st, lib)
+
+
+def kv_restore(k_src, v_src, k_pool, v_pool, batch: PagedBatch, stream=None):
+    """Restore the cached prefixes into the pools: positions 0 .. P_r - 1 of every
+    request from k_src / v_src ([sum P_r][Hkv][D] bf16, request-major). The sources
+    may be pinned host tensors, which the GPU reads directly over PCIe (the cache's
+    CPU tier), or device tensors. This is gc_kv_append with prefix lengths 0 and new
+    lengths P_r; the restore batch's device arrays are built once per PagedBatch."""
+    import torch
+    lib = load_library()
+    for name, t in (("k_src", k_src), ("v_src", v_src)):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise TypeError(f"{name} must be a contiguous bfloat16 tensor")
+        if t.device.type == "cpu" and not t.is_pinned():
+            raise ValueError(f"{name} is in pageable host memory: the GPU reads only pinned host memory")
+        if t.device.type != "cpu" and t.device != batch.device:
+            raise ValueError(f"{name} is on {t.device}, the batch on {batch.device}")
+    for name, t in (("k_pool", k_pool), ("v_pool", v_pool)):
+        _require(t, torch.bfloat16, name, batch.device)
+    if getattr(batch, "_restore", None) is None:
+        batch._restore = PagedBatch(np.zeros_like(batch.prefix_lens), batch.prefix_lens,
+                                    batch.block_tables_host, device=batch.device)
+    rb = batch._restore
+    geo = _geo_from_pools(k_pool, v_pool, k_pool.shape[1], rb)
+    T, Hkv, D = k_src.shape
+    if (T, Hkv, D) != (rb.total_new, geo.num_kv_heads, geo.head_dim) or v_src.shape != k_src.shape:
+        raise ValueError("k_src/v_src must be [sum of prefix lengths][Hkv][D] matching the batch and pools")
+    st = lib.gc_kv_append(ctypes.byref(geo), ctypes.byref(rb.desc()), k_src.data_ptr(), v_src.data_ptr(),
+                          k_pool.data_ptr(), v_pool.data_ptr(), _stream_handle(stream))
+    _check("gc_kv_append (restore)", st, lib)
 
 
 def workspace_size(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_tiles=None,

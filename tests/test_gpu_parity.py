@@ -321,3 +321,37 @@ def test_read_probe_reads_every_word():
     torch.cuda.synchronize()
     nz = torch.nonzero(sink).flatten().tolist()
     assert len(nz) == 1 and int(sink[nz[0]].item()) == 0x5A5A
+
+
+@pytest.mark.parametrize("source", ["pinned_host", "device"])
+def test_restore_prefix_from_host_tier(source):
+    """Restoring every cached prefix into an all-NaN pool (positions 0 .. P_r - 1 written
+    through the append path, sources read over PCIe from pinned host memory) reproduces
+    the oracle's initial pool bit for bit; the new tokens' slots stay NaN."""
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build([300, 0, 33, 1000, 16], [5, 7, 1, 2, 3], 16, 2, 128, seed=320, name="restore")
+    run = H.DeviceRun(w)
+    nan = np.full_like(w.k_pool, W.BF16_NAN)
+    kp = H.to_dev_bf16(nan)
+    vp = H.to_dev_bf16(np.full_like(w.v_pool, W.BF16_NAN))
+    ks = torch.from_numpy(w.k_prefix.view(np.int16)).view(torch.bfloat16)
+    vs = torch.from_numpy(w.v_prefix.view(np.int16)).view(torch.bfloat16)
+    if source == "pinned_host":
+        ks, vs = ks.pin_memory(), vs.pin_memory()
+    else:
+        ks, vs = ks.cuda(), vs.cuda()
+    gc.kv_restore(ks, vs, kp, vp, run.batch)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.from_dev_bits(kp), w.k_pool)
+    assert np.array_equal(H.from_dev_bits(vp), w.v_pool)
+
+
+def test_restore_refuses_pageable_host_memory():
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build([40], [2], 8, 2, 64, seed=321, name="restore_pageable")
+    run = H.DeviceRun(w)
+    ks = torch.from_numpy(w.k_prefix.view(np.int16)).view(torch.bfloat16)
+    with pytest.raises(ValueError):
+        gc.kv_restore(ks, ks, run.k_pool, run.v_pool, run.batch)
