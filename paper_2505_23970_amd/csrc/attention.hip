@@ -235,17 +235,16 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
                 for (int e = 0; e < 16; ++e)
                     s[b][e] = (32 * b + 16 * (e >> 3) + (e & 7) > rel) ? -INFINITY : s[b][e];
         }
-        // tree maximum, then the other half of the lane pair
-        float t8[8];
+        // row maximum: NaN-propagating maxima need no operand canonicalisation and
+        // fold three operands per instruction
+        float mx = s[0][0];
 #pragma unroll
-        for (int x = 0; x < 8; ++x)
-            t8[x] = fmaxf(fmaxf(s[0][2 * x], s[0][2 * x + 1]), fmaxf(s[1][2 * x], s[1][2 * x + 1]));
+        for (int e = 1; e < 16; ++e) mx = __builtin_elementwise_maximum(mx, s[0][e]);
 #pragma unroll
-        for (int x = 0; x < 4; ++x) t8[x] = fmaxf(t8[x], t8[x + 4]);
-        float mx = fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3]));
+        for (int e = 0; e < 16; ++e) mx = __builtin_elementwise_maximum(mx, s[1][e]);
         {
             const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-            mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+            mx = __builtin_elementwise_maximum(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
         }
         const float m_tile = mx * c;
         if (__any(m_tile > m_run + kTileLog2Thresh)) {
