@@ -27,6 +27,7 @@ import numpy as np
 
 BF16_NAN = np.uint16(0x7FC0)
 BF16_ONE = np.uint16(0x3F80)
+E4M3_NAN = np.uint8(0x7F)  # the 8-bit pools' poison (an E4M3 NaN code)
 SEED_BASE = 2505239700
 
 CONFIG_NAMES = {
@@ -243,6 +244,39 @@ def build(prefix_lens, new_lens, num_q_heads, num_kv_heads, head_dim, *, seed,
                     k_pool=None, v_pool=None, scale=1.0 / math.sqrt(D)).finish()
 
 
+
+
+def e4m3_pools(w: Workload, seed: int | None = None):
+    """Initial 8-bit pools for w (same shapes and slots as w.k_pool / w.v_pool,
+    one byte per element): every cached prefix slot holds a random finite E4M3
+    code (sign uniform, exponent field uniform in 2..10, mantissa uniform, so
+    magnitudes 2^-5 .. 15 before the pool scale), every other slot the NaN
+    code. Random codes rather than quantised prefix values keep the method's
+    arithmetic out of this module; the new tokens' K/V stay bf16 and are
+    quantised by the append under test."""
+    rng = np.random.default_rng(w.seed + 8 if seed is None else seed)
+    S, D, Hkv, NB = w.page_size, w.head_dim, w.num_kv_heads, w.num_blocks
+    total_p = int(w.prefix_lens.sum())
+
+    def codes():
+        sign = rng.integers(0, 2, (total_p, Hkv, D)) << 7
+        expo = rng.integers(2, 11, (total_p, Hkv, D)) << 3
+        mant = rng.integers(0, 8, (total_p, Hkv, D))
+        return (sign | expo | mant).astype(np.uint8)
+
+    kc, vc = codes(), codes()
+    kp = np.full((NB, Hkv, S, D), E4M3_NAN, np.uint8)
+    vp = np.full((NB, Hkv, D, S), E4M3_NAN, np.uint8)
+    cup = w.cu_prefix_lens
+    for r in range(w.batch):
+        Pr = int(w.prefix_lens[r])
+        base = int(cup[r])
+        for p in range((Pr + S - 1) // S):
+            blk = int(w.block_tables[r, p])
+            cnt = min(S, Pr - p * S)
+            kp[blk, :, :cnt, :] = kc[base + p * S: base + p * S + cnt].transpose(1, 0, 2)
+            vp[blk, :, :, :cnt] = vc[base + p * S: base + p * S + cnt].transpose(1, 2, 0)
+    return kp, vp
 
 
 def make_config(k: int, seed: int | None = None, values: str = "normal") -> Workload:

@@ -8,7 +8,12 @@ Sources of truth (none of them is the oracle's own code):
   * torch's scaled_dot_product_attention in float64 on the CPU, applied to the
     dense concatenated sequence (prefix ‖ new) — the paper's defining claim
     that reused prefix KV gives the same result as recomputation (§2.2);
-  * invariants: softmax weights sum to 1, block relabelling, chunked turns.
+  * invariants: softmax weights sum to 1, block relabelling, chunked turns;
+  * for the 8-bit pools: the code values the OCP 8-bit floating-point
+    specification prints (tests/golden/e4m3_codes.json), round-to-nearest-even
+    and saturation properties, numpy's float32 product for the quantisation
+    step, and the (independently pinned) bf16 oracle on pools holding the
+    dequantised values.
 """
 from __future__ import annotations
 
@@ -24,6 +29,7 @@ from oracle import bruteforce
 from paper_2505_23970_amd import workloads as W
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
+E4M3_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "e4m3_codes.json")
 
 
 def _value(x):
@@ -177,8 +183,113 @@ def check_position_code(lib):
     return None
 
 
+# ------------------------------------------------------------------ 8-bit pools
+
+def check_e4m3_spec_values(lib):
+    with open(E4M3_GOLDEN) as f:
+        g = json.load(f)
+    for code, val in g["values"].items():
+        got = oracle.e4m3_value(int(code, 16), lib=lib)
+        want = -0.0 if val == "-0" else float(Fraction(val))
+        if got != want or math.copysign(1.0, got) != math.copysign(1.0, want):
+            return f"code {code}: {got} != {want}"
+    for code in g["nan_codes"]:
+        if not math.isnan(oracle.e4m3_value(int(code, 16), lib=lib)):
+            return f"code {code} is not NaN"
+    vals = [oracle.e4m3_value(c, lib=lib) for c in range(127)]
+    if any(not math.isfinite(v) for v in vals) or any(b <= a for a, b in zip(vals, vals[1:])):
+        return "codes 0x00..0x7e are not finite and strictly increasing"
+    for c in range(127):
+        if oracle.e4m3_value(c | 0x80, lib=lib) != -vals[c]:
+            return f"code {c | 0x80:#x} is not the negation of {c:#x}"
+    return None
+
+
+def check_e4m3_rounding(lib):
+    f32 = np.float32
+    vals = [oracle.e4m3_value(c, lib=lib) for c in range(127)]
+    enc = lambda v: oracle.e4m3_encode(v, lib=lib)  # noqa: E731
+    for c in range(127):
+        if enc(vals[c]) != c or enc(-vals[c]) != (c | 0x80):
+            return f"code {c:#x} does not round-trip"
+    for c in range(126):
+        mid = f32((vals[c] + vals[c + 1]) / 2)  # exact: at most 5 significant bits
+        even = c if c % 2 == 0 else c + 1
+        if enc(mid) != even:
+            return f"tie between {c:#x} and {c + 1:#x} went to {enc(mid):#x}"
+        if enc(np.nextafter(mid, f32(np.inf))) != c + 1 or enc(np.nextafter(mid, f32(-np.inf))) != c:
+            return f"values next to the midpoint of {c:#x} and {c + 1:#x} round the wrong way"
+    for v, want in ((464.0, 0x7E), (1e38, 0x7E), (float("inf"), 0x7E), (-float("inf"), 0xFE),
+                    (-500.0, 0xFE), (2.0 ** -10, 0x00), (-(2.0 ** -10), 0x80),
+                    (float(np.nextafter(f32(2.0 ** -10), f32(1))), 0x01)):
+        if enc(v) != want:
+            return f"encode({v}) = {enc(v):#x}, want {want:#x}"
+    return None
+
+
+def check_e4m3_quantize_product(lib):
+    """The bulk quantiser stores encode(fl32(x * fl32(1 / scale))), the product taken
+    by numpy in float32."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    x = W.bf16_bits_to_f32(bits)
+    bits = bits[np.isfinite(x)]
+    x = x[np.isfinite(x)]
+    for scale in (1.0, 0.37, 2.0 ** -7, 3.1 / 448.0):
+        inv = oracle.inv_scale(scale)
+        got = oracle.quantize_e4m3(bits, scale, lib=lib)
+        with np.errstate(over="ignore"):
+            prod = (x * inv).astype(np.float32)
+        idx = np.random.default_rng(5).choice(bits.size, 1500, replace=False)
+        for i in idx:
+            if got[i] != oracle.e4m3_encode(prod[i], lib=lib):
+                return f"scale {scale}: bf16 {bits[i]:#x} quantised to {got[i]:#x}"
+    return None
+
+
+def _dequantised_bf16(codes, scale, lib):
+    table = np.array([oracle.e4m3_value(c, lib=lib) for c in range(256)], np.float64) * scale
+    return W.f32_to_bf16_bits(table[codes].astype(np.float32))
+
+
+def check_e4m3_pools_match_bf16_oracle(lib):
+    """With power-of-two scales every dequantised element is a bf16 value, so the
+    8-bit append and attention must give exactly what the bf16 oracle gives on
+    pools holding those values; different key and value scales catch a swap."""
+    ks, vs = 2.0 ** -6, 2.0 ** -4
+    for P, n, Hq, Hkv, D, seed in (([21, 0, 9], [13, 4, 30], 4, 2, 8, 61),
+                                   ([40], [7], 8, 2, 16, 62)):
+        w = W.build(P, n, Hq, Hkv, D, seed=seed)
+        k8, v8 = W.e4m3_pools(w)
+        kp8, vp8 = oracle.kv_append_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                         w.k_new, w.v_new, k8, v8, ks, vs, lib=lib)
+        # the append wrote exactly the quantised new tokens and nothing else
+        changed = int((kp8 != k8).sum() + (vp8 != v8).sum())
+        want_k = oracle.quantize_e4m3(w.k_new, ks, lib=lib)
+        want_v = oracle.quantize_e4m3(w.v_new, vs, lib=lib)
+        if changed > 2 * w.total_new * Hkv * D:
+            return "8-bit append changed slots it does not own"
+        cu = w.cu_new_lens
+        for r in range(w.batch):
+            for i in range(int(w.new_lens[r])):
+                pos = int(w.prefix_lens[r]) + i
+                blk, off = int(w.block_tables[r, pos // 16]), pos % 16
+                t = int(cu[r]) + i
+                if not (np.array_equal(kp8[blk, :, off, :], want_k[t])
+                        and np.array_equal(vp8[blk, :, :, off], want_v[t])):
+                    return f"8-bit append slot of request {r} token {i} holds other codes"
+        out8, lse8 = oracle.attention_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                           w.q, kp8, vp8, ks, vs, w.scale, lib=lib)
+        out, lse = oracle.attention(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q,
+                                    _dequantised_bf16(kp8, ks, lib), _dequantised_bf16(vp8, vs, lib),
+                                    w.scale, lib=lib)
+        if not (np.array_equal(out8, out) and np.array_equal(lse8, lse)):
+            return f"8-bit attention differs from the bf16 oracle on dequantised pools ({seed})"
+    return None
+
+
 ALL_CHECKS = [check_hand_examples, check_bruteforce, check_prefix_reuse_equals_recompute,
-              check_rows_sum_to_one, check_position_code]
+              check_rows_sum_to_one, check_position_code, check_e4m3_spec_values,
+              check_e4m3_rounding, check_e4m3_quantize_product, check_e4m3_pools_match_bf16_oracle]
 
 
 def run_all(lib):

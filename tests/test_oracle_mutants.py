@@ -42,20 +42,51 @@ MUTANTS = {
         "if (lse) lse[k] = m + log(l);",
         "if (lse) lse[k] = log(l);"),
     "value_page_read_untransposed": (
-        "o[c] += p * widen(v_pool[((blk * num_kv_heads + kvh) * head_dim + c) * page + j % page]);",
-        "o[c] += p * widen(v_pool[((blk * num_kv_heads + kvh) * page + j % page) * head_dim + c]);"),
+        "o[c] += p * kv_elem(v_pool, kv8, v_scale, ((blk * num_kv_heads + kvh) * head_dim + c) * page + j % page);",
+        "o[c] += p * kv_elem(v_pool, kv8, v_scale, ((blk * num_kv_heads + kvh) * page + j % page) * head_dim + c);"),
     "key_slot_off_by_one": (
-        "const uint16_t* kr = k_pool + ((blk * num_kv_heads + kvh) * page + j % page) * head_dim;",
-        "const uint16_t* kr = k_pool + ((blk * num_kv_heads + kvh) * page + (j + 1) % page) * head_dim;"),
+        "int64_t krow = ((blk * num_kv_heads + kvh) * page + j % page) * head_dim;",
+        "int64_t krow = ((blk * num_kv_heads + kvh) * page + (j + 1) % page) * head_dim;"),
     "value_read_from_key_pool": (
-        "o[c] += p * widen(v_pool[((blk * num_kv_heads + kvh) * head_dim + c) * page + j % page]);",
-        "o[c] += p * widen(k_pool[((blk * num_kv_heads + kvh) * page + j % page) * head_dim + c]);"),
+        "o[c] += p * kv_elem(v_pool, kv8, v_scale, ((blk * num_kv_heads + kvh) * head_dim + c) * page + j % page);",
+        "o[c] += p * kv_elem(k_pool, kv8, v_scale, ((blk * num_kv_heads + kvh) * page + j % page) * head_dim + c);"),
     "append_position_off_by_one": (
         "int64_t pos = (int64_t)prefix_lens[r] + i;",
         "int64_t pos = (int64_t)prefix_lens[r] + i + 1;"),
     "append_value_untransposed": (
-        "v_pool[((blk * num_kv_heads + h) * head_dim + c) * page + off] = vs[c];",
-        "v_pool[((blk * num_kv_heads + h) * page + off) * head_dim + c] = vs[c];"),
+        "int64_t vidx = ((blk * num_kv_heads + h) * head_dim + c) * page + off;",
+        "int64_t vidx = ((blk * num_kv_heads + h) * page + off) * head_dim + c;"),
+    # 8-bit pools
+    "e4m3_exponent_bias_8": (
+        "mag = ldexp(1.0 + (double)m / 8.0, e - 7);",
+        "mag = ldexp(1.0 + (double)m / 8.0, e - 8);"),
+    "e4m3_subnormals_with_hidden_bit": (
+        "mag = ldexp((double)m / 8.0, -6);",
+        "mag = ldexp((double)m / 8.0, -7);"),
+    "e4m3_nan_code_finite": (
+        "if (e == 15 && m == 7) return NAN;",
+        "if (e == 16) return NAN;"),
+    "e4m3_ties_to_odd": (
+        "if (d < best_d || (d == best_d && (c & 1) == 0)) {",
+        "if (d < best_d || (d == best_d && (c & 1) == 1)) {"),
+    "e4m3_ties_away_from_zero": (
+        "if (d < best_d || (d == best_d && (c & 1) == 0)) {",
+        "if (d <= best_d) {"),
+    "e4m3_negative_zero_dropped": (
+        "return (uint8_t)(best | (signbit(v) ? 0x80 : 0));",
+        "return (uint8_t)(best | (v < 0 ? 0x80 : 0));"),
+    "quantise_divides_by_inverse": (
+        "return (float)(widen(x) * (double)inv);",
+        "return (float)(widen(x) / (double)inv);"),
+    "dequantise_scale_dropped": (
+        "if (kv8) return gco_e4m3_value(((const uint8_t*)pool)[idx]) * scale;",
+        "if (kv8) return gco_e4m3_value(((const uint8_t*)pool)[idx]);"),
+    "values_dequantised_with_key_scale": (
+        "o[c] += p * kv_elem(v_pool, kv8, v_scale,",
+        "o[c] += p * kv_elem(v_pool, kv8, k_scale,"),
+    "append_values_quantised_with_key_scale": (
+        "((uint8_t*)v_pool)[vidx] = gco_e4m3_encode(scaled32(vs[c], v_inv));",
+        "((uint8_t*)v_pool)[vidx] = gco_e4m3_encode(scaled32(vs[c], k_inv));"),
     "request_lookup_off_by_one": (
         "while (token >= first + new_lens[r]) {",
         "while (token > first + new_lens[r]) {"),

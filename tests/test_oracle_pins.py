@@ -121,3 +121,35 @@ def test_bf16_widening_is_exact(oracle_lib):
     # and the encoder used by the generator rounds to nearest even
     x = np.array([1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -2.5, 3.0e-39], np.float32)
     assert W.f32_to_bf16_bits(x).tolist() == [0x3F80, 0x3F80, 0x3F82, 0xC020, 0x0021]
+
+
+def test_e4m3_code_values_from_the_ocp_table(oracle_lib):
+    assert pins.check_e4m3_spec_values(oracle_lib) is None
+
+
+def test_e4m3_rounding_nearest_even_and_saturating(oracle_lib):
+    assert pins.check_e4m3_rounding(oracle_lib) is None
+
+
+def test_e4m3_quantiser_uses_the_fp32_product(oracle_lib):
+    assert pins.check_e4m3_quantize_product(oracle_lib) is None
+
+
+def test_8bit_pools_match_bf16_oracle_on_power_of_two_scales(oracle_lib):
+    assert pins.check_e4m3_pools_match_bf16_oracle(oracle_lib) is None
+
+
+def test_8bit_scales_enter_linearly(oracle_lib):
+    """Dequantising first means the key scale multiplies every score and the value
+    scale multiplies the output: the result for scales (ks, vs) equals the result
+    for (1, 1) with softmax scale `scale * ks`, times vs."""
+    w = W.build([33, 5], [9, 17], 8, 2, 16, seed=63)
+    k8, v8 = W.e4m3_pools(w)
+    k8, v8 = oracle.kv_append_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                   w.k_new, w.v_new, k8, v8, 0.011, 0.023, lib=oracle_lib)
+    out, lse = oracle.attention_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q,
+                                     k8, v8, 0.011, 0.023, w.scale, lib=oracle_lib)
+    out1, lse1 = oracle.attention_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                       w.q, k8, v8, 1.0, 1.0, w.scale * 0.011, lib=oracle_lib)
+    np.testing.assert_allclose(out, out1 * 0.023, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(lse, lse1, rtol=1e-12, atol=1e-12)
