@@ -173,6 +173,54 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       hipStream_t stream);
 
 /*
+ * 8-bit KV pools. The paper serves its 70B model with 8-bit weights (§6
+ * "Experimental setup"); storing the context cache in 8 bits likewise halves
+ * the memory a cached token takes, so twice the context fits a given pool, and
+ * halves the bytes the memory-bound (decode-like) attention reads.
+ *   Pool layout: as above with one byte per element,
+ *     k_pool8  uint8 [num_blocks][num_kv_heads][page_size][head_dim]
+ *     v_pool8  uint8 [num_blocks][num_kv_heads][head_dim][page_size]
+ *   Each byte is an OCP 8-bit floating-point E4M3 code (sign, 4 exponent bits
+ *   with bias 7, 3 mantissa bits; subnormals m/8 * 2^-6; S.1111.111 is NaN; no
+ *   infinities; magnitudes up to 448) and stands for code_value * scale, with
+ *   one scale for the key pool (k_scale) and one for the value pool (v_scale).
+ *   Scales must be finite, > 0 and have a finite fl32(1 / scale); otherwise
+ *   GC_ERR_BAD_SHAPE.
+ */
+
+/*
+ * gc_kv_append into 8-bit pools: element x (bf16) of a new token's key is
+ * stored as the E4M3 code nearest to v = fl32(x * fl32(1 / k_scale)) after
+ * clamping v to [-448, 448], ties to the even code, -0 as 0x80 (values use
+ * v_scale). A NaN input is stored as a NaN code. Slots, ordering, host/device
+ * sources and errors as gc_kv_append.
+ */
+gc_status gc_kv_append_fp8(const gc_geometry* geo, const gc_batch* batch,
+                           const void* k_new, const void* v_new, float k_scale, float v_scale,
+                           void* k_pool8, void* v_pool8, hipStream_t stream);
+
+/*
+ * gc_prefix_prefill_run over 8-bit pools: the same attention with every key
+ * and value element dequantised first (code value * scale). Plans, workspaces,
+ * tilings and options are the bf16 ones (gc_prefix_prefill_plan and
+ * gc_prefix_prefill_workspace_size serve both).
+ */
+gc_status gc_prefix_prefill_run_fp8(const gc_geometry* geo, const gc_batch* batch,
+                                    const gc_plan_options* opts,
+                                    const void* q, const void* k_pool8, const void* v_pool8,
+                                    float k_scale, float v_scale, float scale, void* out,
+                                    float* lse, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
+/* gc_prefix_prefill_plan followed by gc_prefix_prefill_run_fp8. */
+gc_status gc_prefix_prefill_attention_fp8(const gc_geometry* geo, const gc_batch* batch,
+                                          const gc_plan_options* opts,
+                                          const void* q, const void* k_pool8, const void* v_pool8,
+                                          float k_scale, float v_scale, float scale, void* out,
+                                          float* lse, void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream);
+
+/*
  * Calibration, not part of the attention path: read every byte of `buf`
  * (device memory, `bytes` a multiple of 16) once as a streaming reduction,
  * writing GC_READ_PROBE_SINK_WORDS 32-bit words to `sink` (device). Timing it

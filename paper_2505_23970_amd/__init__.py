@@ -23,7 +23,8 @@ STATUS_NAMES = {0: "GC_OK", -1: "GC_ERR_NULL_ARG", -2: "GC_ERR_BAD_SHAPE", -3: "
                 -4: "GC_ERR_BLOCK_TABLE", -5: "GC_ERR_WORKSPACE", -6: "GC_ERR_HIP"}
 
 EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefill_plan",
-            "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_read_bandwidth_probe",
+            "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_kv_append_fp8",
+            "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_read_bandwidth_probe",
             "gc_status_string")
 READ_PROBE_SINK_WORDS = 2048 * 256
 
@@ -87,6 +88,12 @@ def load_library(path: str | None = None):
     for fn in (lib.gc_prefix_prefill_run, lib.gc_prefix_prefill_attention):
         fn.restype = i32
         fn.argtypes = [G, Bp, O, vp, vp, vp, ctypes.c_float, vp, vp, vp, ctypes.c_size_t, vp]
+    f32 = ctypes.c_float
+    lib.gc_kv_append_fp8.restype = i32
+    lib.gc_kv_append_fp8.argtypes = [G, Bp, vp, vp, f32, f32, vp, vp, vp]
+    for fn in (lib.gc_prefix_prefill_run_fp8, lib.gc_prefix_prefill_attention_fp8):
+        fn.restype = i32
+        fn.argtypes = [G, Bp, O, vp, vp, vp, f32, f32, f32, vp, vp, vp, ctypes.c_size_t, vp]
     lib.gc_read_bandwidth_probe.restype = i32
     lib.gc_read_bandwidth_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
     lib.gc_status_string.restype = ctypes.c_char_p
@@ -251,11 +258,12 @@ def alloc_workspace(num_q_heads, k_pool, v_pool, batch: PagedBatch, kv_split_til
     return torch.empty(max(n, 256), dtype=torch.uint8, device=batch.device)
 
 
-def _attn_args(q, k_pool, v_pool, batch, out, lse, workspace):
+def _attn_args(q, k_pool, v_pool, batch, out, lse, workspace, pool_dtype=None):
     import torch
+    pool_dtype = pool_dtype or torch.bfloat16
     _require(q, torch.bfloat16, "q", batch.device)
-    _require(k_pool, torch.bfloat16, "k_pool", batch.device)
-    _require(v_pool, torch.bfloat16, "v_pool", batch.device)
+    _require(k_pool, pool_dtype, "k_pool", batch.device)
+    _require(v_pool, pool_dtype, "v_pool", batch.device)
     T, Hq, D = q.shape
     geo = _geo_from_pools(k_pool, v_pool, Hq, batch)
     if T != batch.total_new or D != geo.head_dim:
@@ -331,4 +339,60 @@ def prefix_prefill_attention(q, k_pool, v_pool, batch: PagedBatch, scale, worksp
                                          workspace.data_ptr(), workspace.numel(),
                                          _stream_handle(stream))
     _check("gc_prefix_prefill_attention", st, lib)
+    return out
+
+
+# ----------------------------------------------------------------- 8-bit (E4M3) pools
+# Pools are uint8 tensors of E4M3 codes with the bf16 pools' shapes; each pool has
+# one scale (element = code value * scale). See include/greencache.h.
+
+def kv_append_fp8(k_new, v_new, k_pool8, v_pool8, batch: PagedBatch, k_scale, v_scale, stream=None):
+    """Quantise the new tokens' K/V ([T][Hkv][D] bf16) into the 8-bit pools in place."""
+    import torch
+    lib = load_library()
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _require(t, torch.bfloat16, name, batch.device)
+    for name, t in (("k_pool8", k_pool8), ("v_pool8", v_pool8)):
+        _require(t, torch.uint8, name, batch.device)
+    geo = _geo_from_pools(k_pool8, v_pool8, k_pool8.shape[1], batch)
+    T, Hkv, D = k_new.shape
+    if (T, Hkv, D) != (batch.total_new, geo.num_kv_heads, geo.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [T][Hkv][D] matching the batch and pools")
+    st = lib.gc_kv_append_fp8(ctypes.byref(geo), ctypes.byref(batch.desc()), k_new.data_ptr(),
+                              v_new.data_ptr(), float(k_scale), float(v_scale), k_pool8.data_ptr(),
+                              v_pool8.data_ptr(), _stream_handle(stream))
+    _check("gc_kv_append_fp8", st, lib)
+
+
+def run_fp8(q, k_pool8, v_pool8, batch: PagedBatch, scale, k_scale, v_scale, workspace, out=None,
+            lse=None, kv_split_tiles=None, stream=None, tiling=None):
+    import torch
+    lib = load_library()
+    geo, out = _attn_args(q, k_pool8, v_pool8, batch, out, lse, workspace, torch.uint8)
+    st = lib.gc_prefix_prefill_run_fp8(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                       _opts(kv_split_tiles, tiling), q.data_ptr(), k_pool8.data_ptr(),
+                                       v_pool8.data_ptr(), float(k_scale), float(v_scale), float(scale),
+                                       out.data_ptr(), lse.data_ptr() if lse is not None else None,
+                                       workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    _check("gc_prefix_prefill_run_fp8", st, lib)
+    return out
+
+
+def prefix_prefill_attention_fp8(q, k_pool8, v_pool8, batch: PagedBatch, scale, k_scale, v_scale,
+                                 workspace=None, out=None, lse=None, kv_split_tiles=None,
+                                 stream=None, tiling=None):
+    """prefix_prefill_attention over 8-bit pools (uint8 E4M3 codes, one scale per pool)."""
+    import torch
+    lib = load_library()
+    if workspace is None:
+        workspace = alloc_workspace(q.shape[1], k_pool8, v_pool8, batch, kv_split_tiles, tiling)
+    geo, out = _attn_args(q, k_pool8, v_pool8, batch, out, lse, workspace, torch.uint8)
+    st = lib.gc_prefix_prefill_attention_fp8(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                             _opts(kv_split_tiles, tiling), q.data_ptr(),
+                                             k_pool8.data_ptr(), v_pool8.data_ptr(), float(k_scale),
+                                             float(v_scale), float(scale), out.data_ptr(),
+                                             lse.data_ptr() if lse is not None else None,
+                                             workspace.data_ptr(), workspace.numel(),
+                                             _stream_handle(stream))
+    _check("gc_prefix_prefill_attention_fp8", st, lib)
     return out

@@ -226,9 +226,15 @@ gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& s
     return gc::launch_plan(a, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
 }
 
+// Pools of bf16 elements (fp8 false, scales 1) or of E4M3 codes with one scale each.
+struct PoolKind {
+    bool fp8 = false;
+    float k_scale = 1.f, v_scale = 1.f;
+};
+
 gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
                       const void* q, const void* k_pool, const void* v_pool, float scale,
-                      void* out, float* lse, void* ws, hipStream_t stream) {
+                      void* out, float* lse, void* ws, hipStream_t stream, const PoolKind& pk = PoolKind{}) {
     gc::AttnArgs a{};
     a.q = static_cast<const uint16_t*>(q);
     a.k_pool = static_cast<const uint16_t*>(k_pool);
@@ -247,9 +253,10 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
     a.tq = sh.tq;
     a.num_blocks = geo->num_blocks;
     a.max_blocks = geo->max_blocks_per_seq;
-    a.scale_log2 = (float)((double)scale * 1.4426950408889634074);
-    const hipError_t e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, stream)
-                                  : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, stream);
+    a.scale_log2 = (float)((double)scale * (double)pk.k_scale * 1.4426950408889634074);
+    a.v_scale = pk.v_scale;
+    const hipError_t e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, pk.fp8, stream)
+                                  : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, pk.fp8, stream);
     if (e != hipSuccess) return GC_ERR_HIP;
     if (pl.combines > 0) {
         gc::CombineArgs c{};
@@ -280,18 +287,21 @@ gc_status check_run_args(const void* q, const void* k_pool, const void* v_pool, 
     return GC_OK;
 }
 
+gc_status check_pool_scales(float k_scale, float v_scale) {
+    if (!std::isfinite(k_scale) || !(k_scale > 0.f) || !std::isfinite(v_scale) || !(v_scale > 0.f))
+        return GC_ERR_BAD_SHAPE;
+    // the append multiplies by fl32(1 / scale), which must be finite as well
+    if (!std::isfinite(1.f / k_scale) || !std::isfinite(1.f / v_scale)) return GC_ERR_BAD_SHAPE;
+    return GC_OK;
+}
+
 gc_status check_workspace(const Plan& pl, const void* ws, size_t bytes) {
     if (ws == nullptr || bytes < pl.layout.total) return GC_ERR_WORKSPACE;
     return GC_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-__attribute__((visibility("default")))
-gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch, const void* k_new,
-                       const void* v_new, void* k_pool, void* v_pool, hipStream_t stream) {
+gc_status append(const gc_geometry* geo, const gc_batch* batch, const void* k_new, const void* v_new,
+                 void* k_pool, void* v_pool, const PoolKind& pk, hipStream_t stream) {
     Shape sh;
     gc_status st = check_common(geo, batch, &sh);
     if (st != GC_OK) return st;
@@ -301,8 +311,8 @@ gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch, const void
     gc::AppendArgs a{};
     a.k_new = static_cast<const uint16_t*>(k_new);
     a.v_new = static_cast<const uint16_t*>(v_new);
-    a.k_pool = static_cast<uint16_t*>(k_pool);
-    a.v_pool = static_cast<uint16_t*>(v_pool);
+    a.k_pool = k_pool;
+    a.v_pool = v_pool;
     a.prefix_lens = batch->prefix_lens_dev;
     a.cu_new_lens = batch->cu_new_lens_dev;
     a.block_tables = batch->block_tables_dev;
@@ -311,7 +321,51 @@ gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch, const void
     a.num_kv_heads = geo->num_kv_heads;
     a.num_blocks = geo->num_blocks;
     a.max_blocks = geo->max_blocks_per_seq;
-    return gc::launch_append(a, geo->head_dim, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+    a.k_inv = 1.f / pk.k_scale;  // IEEE division: the same fl32(1 / scale) the definition uses
+    a.v_inv = 1.f / pk.v_scale;
+    return gc::launch_append(a, geo->head_dim, pk.fp8, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+}
+
+gc_status run(const gc_geometry* geo, const gc_batch* batch, const gc_plan_options* opts,
+              const void* q, const void* k_pool, const void* v_pool, float scale, void* out,
+              float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream,
+              bool with_plan, const PoolKind& pk) {
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    st = check_run_args(q, k_pool, v_pool, scale, out);
+    if (st != GC_OK) return st;
+    if (pk.fp8) {
+        st = check_pool_scales(pk.k_scale, pk.v_scale);
+        if (st != GC_OK) return st;
+    }
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != GC_OK) return st;
+    if (with_plan) {
+        st = enqueue_plan(geo, batch, sh, pl, workspace, stream);
+        if (st != GC_OK) return st;
+    }
+    return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream, pk);
+}
+
+}  // namespace
+
+extern "C" {
+
+__attribute__((visibility("default")))
+gc_status gc_kv_append(const gc_geometry* geo, const gc_batch* batch, const void* k_new,
+                       const void* v_new, void* k_pool, void* v_pool, hipStream_t stream) {
+    return append(geo, batch, k_new, v_new, k_pool, v_pool, PoolKind{}, stream);
+}
+
+__attribute__((visibility("default")))
+gc_status gc_kv_append_fp8(const gc_geometry* geo, const gc_batch* batch, const void* k_new,
+                           const void* v_new, float k_scale, float v_scale, void* k_pool,
+                           void* v_pool, hipStream_t stream) {
+    const gc_status st = check_pool_scales(k_scale, v_scale);
+    if (st != GC_OK) return st;
+    return append(geo, batch, k_new, v_new, k_pool, v_pool, PoolKind{true, k_scale, v_scale}, stream);
 }
 
 __attribute__((visibility("default")))
@@ -344,15 +398,8 @@ gc_status gc_prefix_prefill_run(const gc_geometry* geo, const gc_batch* batch,
                                 const gc_plan_options* opts, const void* q, const void* k_pool,
                                 const void* v_pool, float scale, void* out, float* lse,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    Shape sh;
-    Plan pl;
-    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
-    if (st != GC_OK || sh.total_tokens == 0) return st;
-    st = check_run_args(q, k_pool, v_pool, scale, out);
-    if (st != GC_OK) return st;
-    st = check_workspace(pl, workspace, workspace_bytes);
-    if (st != GC_OK) return st;
-    return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream);
+    return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
+               stream, false, PoolKind{});
 }
 
 __attribute__((visibility("default")))
@@ -361,17 +408,29 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       const void* k_pool, const void* v_pool, float scale,
                                       void* out, float* lse, void* workspace,
                                       size_t workspace_bytes, hipStream_t stream) {
-    Shape sh;
-    Plan pl;
-    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
-    if (st != GC_OK || sh.total_tokens == 0) return st;
-    st = check_run_args(q, k_pool, v_pool, scale, out);
-    if (st != GC_OK) return st;
-    st = check_workspace(pl, workspace, workspace_bytes);
-    if (st != GC_OK) return st;
-    st = enqueue_plan(geo, batch, sh, pl, workspace, stream);
-    if (st != GC_OK) return st;
-    return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream);
+    return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
+               stream, true, PoolKind{});
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_run_fp8(const gc_geometry* geo, const gc_batch* batch,
+                                    const gc_plan_options* opts, const void* q, const void* k_pool,
+                                    const void* v_pool, float k_scale, float v_scale, float scale,
+                                    void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+    return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
+               stream, false, PoolKind{true, k_scale, v_scale});
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_attention_fp8(const gc_geometry* geo, const gc_batch* batch,
+                                          const gc_plan_options* opts, const void* q,
+                                          const void* k_pool, const void* v_pool, float k_scale,
+                                          float v_scale, float scale, void* out, float* lse,
+                                          void* workspace, size_t workspace_bytes,
+                                          hipStream_t stream) {
+    return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
+               stream, true, PoolKind{true, k_scale, v_scale});
 }
 
 __attribute__((visibility("default")))

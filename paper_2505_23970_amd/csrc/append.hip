@@ -9,14 +9,36 @@
 // tokens' rows are staged in LDS and written out column-wise, so the 16 lanes
 // that write one page row touch 32 consecutive bytes when the tokens share a
 // page. Slots whose block id is missing or outside the pool are skipped.
+// 8-bit pools store E4M3 codes: each element x becomes the code nearest to
+// fl32(x * inv) clamped to [-448, 448] (ties to even; the conversion
+// instruction rounds to nearest even, the clamp makes it saturate).
 #include "gc_internal.h"
 
 namespace gc {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-template <int D>
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+// Saturate to the largest E4M3 magnitude; NaN stays NaN (and converts to a NaN code).
+__device__ __forceinline__ float clamp448(float x) {
+    return __builtin_isnan(x) ? x : fminf(fmaxf(x, -448.f), 448.f);
+}
+
+// Four bf16 values (two words) as four E4M3 codes (one word, first value lowest).
+__device__ __forceinline__ uint32_t quantise4(uint32_t w0, uint32_t w1, float inv) {
+    int r = __builtin_amdgcn_cvt_pk_fp8_f32(clamp448(bf16_lo(w0) * inv), clamp448(bf16_hi(w0) * inv), 0, false);
+    r = __builtin_amdgcn_cvt_pk_fp8_f32(clamp448(bf16_lo(w1) * inv), clamp448(bf16_hi(w1) * inv), r, true);
+    return (uint32_t)r;
+}
+__device__ __forceinline__ uint8_t quantise1(uint16_t x, float inv) {
+    const float v = clamp448(__uint_as_float((uint32_t)x << 16) * inv);
+    return (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(v, v, 0, false) & 0xFF);
+}
+
+template <int D, bool FP8>
 __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendArgs a) {
     constexpr int CPR = D / 8;        // 16-byte chunks per row
     constexpr int kStride = D + 8;    // padded LDS row (elements)
@@ -61,7 +83,12 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendArgs
             const int blk = s_blk[tl];
             if (blk >= 0) {
                 const u32x4 k = *reinterpret_cast<const u32x4*>(a.k_new + src);
-                *reinterpret_cast<u32x4*>(a.k_pool + (((int64_t)blk * a.num_kv_heads + h) * kPage + s_off[tl]) * D + ch * 8) = k;
+                const int64_t dst = (((int64_t)blk * a.num_kv_heads + h) * kPage + s_off[tl]) * D + ch * 8;
+                if constexpr (FP8)
+                    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(a.k_pool) + dst) =
+                        u32x2{quantise4(k[0], k[1], a.k_inv), quantise4(k[2], k[3], a.k_inv)};
+                else
+                    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.k_pool) + dst) = k;
             }
             v = *reinterpret_cast<const u32x4*>(a.v_new + src);
         }
@@ -71,19 +98,31 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendArgs
     for (int x = tid; x < kAppendTokens * D; x += kAppendThreads) {
         const int tl = x % kAppendTokens, d = x / kAppendTokens;
         const int blk = s_blk[tl];
-        if (tl < ntok && blk >= 0)
-            a.v_pool[(((int64_t)blk * a.num_kv_heads + h) * D + d) * kPage + s_off[tl]] = s_v[tl * kStride + d];
+        if (tl < ntok && blk >= 0) {
+            const int64_t dst = (((int64_t)blk * a.num_kv_heads + h) * D + d) * kPage + s_off[tl];
+            if constexpr (FP8)
+                static_cast<uint8_t*>(a.v_pool)[dst] = quantise1(s_v[tl * kStride + d], a.v_inv);
+            else
+                static_cast<uint16_t*>(a.v_pool)[dst] = s_v[tl * kStride + d];
+        }
     }
 }
 
 }  // namespace
 
-hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s) {
+hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t s) {
     const dim3 grid((unsigned)ceil_div(a.total_tokens, kAppendTokens), (unsigned)a.num_kv_heads);
-    if (head_dim == 128)
-        append_kernel<128><<<grid, kAppendThreads, 0, s>>>(a);
-    else
-        append_kernel<64><<<grid, kAppendThreads, 0, s>>>(a);
+    if (fp8) {
+        if (head_dim == 128)
+            append_kernel<128, true><<<grid, kAppendThreads, 0, s>>>(a);
+        else
+            append_kernel<64, true><<<grid, kAppendThreads, 0, s>>>(a);
+    } else {
+        if (head_dim == 128)
+            append_kernel<128, false><<<grid, kAppendThreads, 0, s>>>(a);
+        else
+            append_kernel<64, false><<<grid, kAppendThreads, 0, s>>>(a);
+    }
     return hipGetLastError();
 }
 

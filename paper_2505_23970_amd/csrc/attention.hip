@@ -26,6 +26,11 @@
 // inline assembly with explicit waits, so the compiler's own LDS waits count
 // only LDS reads and can keep several fragment reads in flight per MFMA
 // (scheduling fences hold that order).
+// 8-bit pools (E4M3 codes times one scale per pool): the next tile's codes are
+// loaded into registers instead, widened to bf16 (exact) and written to the same
+// LDS layout after the current tile's products, so the compute loop is shared;
+// the key scale is folded into the softmax scale, the value scale into the
+// final normalisation.
 #include "gc_internal.h"
 
 namespace gc {
@@ -78,7 +83,19 @@ __device__ __forceinline__ void wait_vmem() {
     asm volatile("" ::: "memory");  // no LDS access moves above the wait
 }
 
-template <int D, int WAVES>
+// Sixteen E4M3 codes (four words) as sixteen bf16 values (eight words).
+__device__ __forceinline__ void widen_e4m3x16(const u32x4 c, u32x4& lo, u32x4& hi) {
+    uint32_t w[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        w[2 * i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[i], 1.0f, false));
+        w[2 * i + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(c[i], 1.0f, true));
+    }
+    lo = u32x4{w[0], w[1], w[2], w[3]};
+    hi = u32x4{w[4], w[5], w[6], w[7]};
+}
+
+template <int D, int WAVES, bool FP8>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const AttnArgs a) {
     constexpr int kBlockRows = WAVES * kRowsPerWave;  // query rows of a work item
     constexpr int DK = D / 16;                      // k-steps of QK^T
@@ -194,7 +211,9 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
     const int prow = (lr & 0x13) | ((lr & 4) << 1) | ((lr & 8) >> 1);
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-    constexpr int kAhead = 6;  // LDS fragment reads kept in flight ahead of their MFMA
+    // LDS fragment reads kept in flight ahead of their MFMA (fewer when 8-bit codes
+    // for the next tile occupy registers during the products)
+    constexpr int kAhead = (FP8 && WAVES == 4 && D == 128) ? 4 : 6;
     auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt) {
         // S^T = K_tile . Q^T: MFMA i uses K fragment (k = i/2, block b = i%2). Every
         // group below is fenced so the fragment reads stay kAhead MFMAs ahead.
@@ -292,6 +311,77 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
         }
     };
 
+    // 8-bit pools: 16-byte chunks of codes. Chunk c of the K tile is key row
+    // c / (D/16), codes 16 (c % (D/16)) ..; chunk c of the V tile is value row c % D
+    // of page c / D (16 keys). Lane chunk e is c = 64 (WAVES e + wave) + lane, so a
+    // wave's chunks of one e lie in one page.
+    constexpr int kChunks = 4 * D;                                   // per tensor and tile
+    constexpr int NC = (kChunks + WAVES * 64 - 1) / (WAVES * 64);   // per lane
+    const int64_t page_codes = (int64_t)kPage * D;                   // bytes of an 8-bit page
+    const int64_t block_codes = (int64_t)a.num_kv_heads * page_codes;
+    u32x4 kc8[NC], vc8[NC];
+    auto load8 = [&](int kt, const int ids) {
+#pragma unroll
+        for (int e = 0; e < NC; ++e) {
+            const int c0 = 64 * (WAVES * e + wave);  // the wave's first chunk
+            const int c = c0 + lane;
+            if (c0 < kChunks) {
+                const int kpg = (c0 / (D / 16)) / kPage;
+                const int vpg = c0 / D;
+                int kb = __builtin_amdgcn_readlane(ids, kpg), vb = __builtin_amdgcn_readlane(ids, vpg);
+                // pages past the table, past the sequence or with a bad id read block 0
+                // (their keys are masked and their values zeroed below)
+                const bool kok = kt * 4 + kpg < a.max_blocks && (kt * 4 + kpg) * kPage < L &&
+                                 kb >= 0 && kb < a.num_blocks;
+                const bool vok = kt * 4 + vpg < a.max_blocks && (kt * 4 + vpg) * kPage < L &&
+                                 vb >= 0 && vb < a.num_blocks;
+                kb = kok ? kb : 0;
+                vb = vok ? vb : 0;
+                const uint8_t* kp = reinterpret_cast<const uint8_t*>(a.k_pool) + kb * block_codes +
+                                    kvh * page_codes + (c / (D / 16)) % kPage * D + (c % (D / 16)) * 16;
+                const uint8_t* vp = reinterpret_cast<const uint8_t*>(a.v_pool) + vb * block_codes +
+                                    kvh * page_codes + (c % D) * kPage;
+                kc8[e] = *reinterpret_cast<const u32x4*>(kp);
+                vc8[e] = *reinterpret_cast<const u32x4*>(vp);
+            }
+        }
+    };
+    auto store8 = [&](unsigned char* kdst, unsigned char* vdst, int kt) {
+        const int first_bad = L - kt * kBlockN;  // tile-relative key index
+#pragma unroll
+        for (int e = 0; e < NC; ++e) {
+            const int c = 64 * (WAVES * e + wave) + lane;
+            if (c < kChunks) {
+                u32x4 lo, hi;
+                widen_e4m3x16(kc8[e], lo, hi);
+                const int kr = c / (D / 16), c8 = c % (D / 16);
+                *reinterpret_cast<u32x4*>(kdst + kr * (2 * D) + swz_k<D>(2 * c8, kr) * 16) = lo;
+                *reinterpret_cast<u32x4*>(kdst + kr * (2 * D) + swz_k<D>(2 * c8 + 1, kr) * 16) = hi;
+                widen_e4m3x16(vc8[e], lo, hi);
+                const int pg = c / D, d = c % D;
+                const int key0 = pg * kPage;
+                if (key0 + kPage > first_bad) {
+#pragma unroll
+                    for (int x = 0; x < 8; ++x) {
+                        const uint32_t keep = (key0 + x < first_bad ? 0xFFFFu : 0u);
+                        const uint32_t keep8 = (key0 + 8 + x < first_bad ? 0xFFFFu : 0u);
+                        if (x % 2 == 0) {
+                            lo[x / 2] &= keep | 0xFFFF0000u;
+                            hi[x / 2] &= keep8 | 0xFFFF0000u;
+                        } else {
+                            lo[x / 2] &= (keep << 16) | 0xFFFFu;
+                            hi[x / 2] &= (keep8 << 16) | 0xFFFFu;
+                        }
+                    }
+                }
+                unsigned char* vrow = vdst + pg * kPageBytes + d * 32;
+                const int sw = (d >> 3) & 1;
+                *reinterpret_cast<u32x4*>(vrow + sw * 16) = lo;
+                *reinterpret_cast<u32x4*>(vrow + (sw ^ 1) * 16) = hi;
+            }
+        }
+    };
+
     // One pipeline step: start the next tile's loads into the other buffers, compute
     // this tile, make the next tile visible.
     int ids;
@@ -299,22 +389,33 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
     auto step = [&](unsigned char* kc, unsigned char* vc, unsigned char* kn, unsigned char* vn) {
         const bool more = kt + 1 < it.kt_end;
         if (more) {
-            issue_tile(kn, vn, kt + 1, ids);
+            if constexpr (FP8) load8(kt + 1, ids);
+            else issue_tile(kn, vn, kt + 1, ids);
             if (kt + 2 < it.kt_end) fetch_ids(kt + 2, ids);
         }
         compute_tile(kc, vc, kt);
         if (more) {
-            wait_vmem<0>();
-            zero_tail(vn, kt + 1);
+            if constexpr (FP8) {
+                store8(kn, vn, kt + 1);
+            } else {
+                wait_vmem<0>();
+                zero_tail(vn, kt + 1);
+            }
         }
         __syncthreads();
     };
 
     fetch_ids(kt, ids);
-    issue_tile(k_lds0, v_lds0, kt, ids);
-    if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
-    wait_vmem<0>();
-    zero_tail(v_lds0, kt);
+    if constexpr (FP8) {
+        load8(kt, ids);
+        if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
+        store8(k_lds0, v_lds0, kt);
+    } else {
+        issue_tile(k_lds0, v_lds0, kt, ids);
+        if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
+        wait_vmem<0>();
+        zero_tail(v_lds0, kt);
+    }
     __syncthreads();
     while (true) {
         step(k_lds0, v_lds0, k_lds1, v_lds1);
@@ -324,7 +425,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
     }
 
     const float l_tot = l_run + __shfl_xor(l_run, 32);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float inv = l_tot > 0.f ? a.v_scale / l_tot : 0.f;  // v_scale is 1 for bf16 pools
     const float lse_v = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     // o[db][4j + i] is element d = 32db + 8j + 4hh + i of this lane's row
     if (it.part < 0) {
@@ -427,19 +528,28 @@ __global__ __launch_bounds__(kCombineThreads) void combine_kernel(const CombineA
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, hipStream_t s) {
-    const dim3 grid((unsigned)(num_items * a.num_kv_heads));
+template <bool FP8>
+static void launch_prefill(const AttnArgs& a, int head_dim, const dim3 grid, bool wide, hipStream_t s) {
     if (wide) {
         if (head_dim == 128)
-            attention_kernel<128, kWideWaves><<<grid, kWideWaves * 64, 0, s>>>(a);
+            attention_kernel<128, kWideWaves, FP8><<<grid, kWideWaves * 64, 0, s>>>(a);
         else
-            attention_kernel<64, kWideWaves><<<grid, kWideWaves * 64, 0, s>>>(a);
+            attention_kernel<64, kWideWaves, FP8><<<grid, kWideWaves * 64, 0, s>>>(a);
     } else {
         if (head_dim == 128)
-            attention_kernel<128, kWaves><<<grid, kWaves * 64, 0, s>>>(a);
+            attention_kernel<128, kWaves, FP8><<<grid, kWaves * 64, 0, s>>>(a);
         else
-            attention_kernel<64, kWaves><<<grid, kWaves * 64, 0, s>>>(a);
+            attention_kernel<64, kWaves, FP8><<<grid, kWaves * 64, 0, s>>>(a);
     }
+}
+
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
+                            hipStream_t s) {
+    const dim3 grid((unsigned)(num_items * a.num_kv_heads));
+    if (fp8)
+        launch_prefill<true>(a, head_dim, grid, wide, s);
+    else
+        launch_prefill<false>(a, head_dim, grid, wide, s);
     return hipGetLastError();
 }
 

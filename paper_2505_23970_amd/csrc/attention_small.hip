@@ -15,6 +15,10 @@
 // Score block b covers page b of the tile; the k order of the PV product is
 // permuted to match, so the score accumulators are already laid out as the P^T
 // operand and every global load reads a single page.
+// With 8-bit pools (E4M3 codes times one scale per pool) the same fragments are
+// loaded at half the width and widened to bf16 in registers (exact: every E4M3
+// value is a bf16 value); the key scale is folded into the softmax scale and the
+// value scale into the final normalisation, so the loop is otherwise unchanged.
 #include "gc_internal.h"
 
 namespace gc {
@@ -50,7 +54,36 @@ __device__ __forceinline__ float row_sum4(float x) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Four E4M3 codes (one 32-bit word) as four bf16 values (two 32-bit words).
+__device__ __forceinline__ u32x2 widen_e4m3x4(uint32_t w) {
+    const bf16x2 lo = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false);
+    const bf16x2 hi = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true);
+    return u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+}
+
+// Register fragments of one key tile: K^T operands per (page, k-step) and four
+// value slots per (page, value block), at the pool's element width.
+template <int D, bool FP8>
+struct SmallFrags;
 template <int D>
+struct SmallFrags<D, false> {
+    bf16x8 k[2][D / 32];
+    u32x2 v[2][D / 16];
+    __device__ __forceinline__ bf16x8 kop(int b, int s) const { return k[b][s]; }
+    __device__ __forceinline__ u32x2 vop(int b, int db) const { return v[b][db]; }
+};
+template <int D>
+struct SmallFrags<D, true> {
+    u32x2 k[2][D / 32];      // 8 codes
+    uint32_t v[2][D / 16];   // 4 codes
+    __device__ __forceinline__ bf16x8 kop(int b, int s) const {
+        const u32x2 a = widen_e4m3x4(k[b][s][0]), c = widen_e4m3x4(k[b][s][1]);
+        return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], c[0], c[1]});
+    }
+    __device__ __forceinline__ u32x2 vop(int b, int db) const { return widen_e4m3x4(v[b][db]); }
+};
+
+template <int D, bool FP8>
 __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(const AttnArgs a, int64_t units) {
     constexpr int KS = D / 32;                    // k-steps of QK^T
     constexpr int DB = D / 16;                    // 16-row blocks of O^T
@@ -94,17 +127,15 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
     // pages. Every load reads one page, at a wave-uniform page address plus a
     // per-lane offset.
     const scalar_i32p table = (scalar_i32p)(a.block_tables + (int64_t)r * a.max_blocks);
-    const int64_t page_bytes = (int64_t)kPage * D * 2;
+    constexpr int EB = FP8 ? 1 : 2;  // bytes per pool element
+    const int64_t page_bytes = (int64_t)kPage * D * EB;
     const int64_t block_bytes = (int64_t)a.num_kv_heads * page_bytes;
     const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k_pool) + (int64_t)kvh * page_bytes;
     const unsigned char* vbase = reinterpret_cast<const unsigned char*>(a.v_pool) + (int64_t)kvh * page_bytes;
-    const uint32_t k_off = (uint32_t)(j * D + 8 * g4) * 2;          // + 64 s bytes per k-step
-    const uint32_t v_off = (uint32_t)(j * kPage + 4 * g4) * 2;      // + 512 db bytes per value block
+    const uint32_t k_off = (uint32_t)(j * D + 8 * g4) * EB;         // + 32 EB s bytes per k-step
+    const uint32_t v_off = (uint32_t)(j * kPage + 4 * g4) * EB;     // + 256 EB db bytes per value block
 
-    struct Frags {
-        bf16x8 k[2][KS];
-        u32x2 v[2][DB];   // [page][value block]: four bf16 values
-    };
+    using Frags = SmallFrags<D, FP8>;
     // Block ids of the two pages of tile kt (scalar loads, fetched a tile ahead of
     // their use); pages past the sequence end or with an out-of-range id read
     // block 0 instead (their keys are masked, values zeroed).
@@ -131,12 +162,21 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
                 (void*)(kbase + blk[b] * block_bytes), (short)0, (int)page_bytes, kBufferFlags);
             const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
                 (void*)(vbase + blk[b] * block_bytes), (short)0, (int)page_bytes, kBufferFlags);
+            if constexpr (FP8) {
 #pragma unroll
-            for (int s = 0; s < KS; ++s)
-                f.k[b][s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(kr, (int)k_off + 64 * s, 0, 0));
+                for (int s = 0; s < KS; ++s)
+                    f.k[b][s] = __builtin_amdgcn_raw_buffer_load_b64(kr, (int)k_off + 32 * s, 0, 0);
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
-                f.v[b][db] = __builtin_amdgcn_raw_buffer_load_b64(vr, (int)v_off + 512 * db, 0, 0);
+                for (int db = 0; db < DB; ++db)
+                    f.v[b][db] = __builtin_amdgcn_raw_buffer_load_b32(vr, (int)v_off + 256 * db, 0, 0);
+            } else {
+#pragma unroll
+                for (int s = 0; s < KS; ++s)
+                    f.k[b][s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(kr, (int)k_off + 64 * s, 0, 0));
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+                    f.v[b][db] = __builtin_amdgcn_raw_buffer_load_b64(vr, (int)v_off + 512 * db, 0, 0);
+            }
         }
     };
 
@@ -155,8 +195,14 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
             s[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
-                s[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.k[b][ks], qf[ks], s[b], 0, 0, 0);
+                s[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.kop(b, ks), qf[ks], s[b], 0, 0, 0);
         }
+        // value fragments as bf16 words (widened here for 8-bit pools)
+        u32x2 vw[2][DB];
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int db = 0; db < DB; ++db) vw[b][db] = f.vop(b, db);
         // s[b][v] is the score of tile key 16 b + 4 g4 + v
         const int key0 = kt * kDecN;
         if (key0 + kDecN - 1 > P + it.q0) {
@@ -174,8 +220,8 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
                     for (int db = 0; db < DB; ++db)
 #pragma unroll
                         for (int x = 0; x < 2; ++x)
-                            f.v[b][db][x] &= (16 * b + 2 * x < bad ? 0xFFFFu : 0u) |
-                                             (16 * b + 2 * x + 1 < bad ? 0xFFFF0000u : 0u);
+                            vw[b][db][x] &= (16 * b + 2 * x < bad ? 0xFFFFu : 0u) |
+                                            (16 * b + 2 * x + 1 < bad ? 0xFFFF0000u : 0u);
             }
         }
         float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
@@ -203,8 +249,8 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
         const bf16x8 pf = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            const u32x4 vw = {f.v[0][db][0], f.v[0][db][1], f.v[1][db][0], f.v[1][db][1]};
-            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vw), pf, o[db], 0, 0, 0);
+            const u32x4 vv = {vw[0][db][0], vw[0][db][1], vw[1][db][0], vw[1][db][1]};
+            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv), pf, o[db], 0, 0, 0);
         }
     };
 
@@ -233,7 +279,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
     }
 
     const float l_tot = row_sum4(l_run);
-    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    const float inv = l_tot > 0.f ? a.v_scale / l_tot : 0.f;  // v_scale is 1 for bf16 pools
     const float lse_v = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     // o[db][v] is element d = 16 db + 4 g4 + v of row j
     if (it.part < 0) {
@@ -259,13 +305,21 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
 
 }  // namespace
 
-hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s) {
+hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, bool fp8,
+                                  hipStream_t s) {
     const int64_t units = num_items * a.num_kv_heads;
     const dim3 grid((unsigned)ceil_div64(units, kDecWaves));
-    if (head_dim == 128)
-        attention_small_kernel<128><<<grid, kDecWaves * 64, 0, s>>>(a, units);
-    else
-        attention_small_kernel<64><<<grid, kDecWaves * 64, 0, s>>>(a, units);
+    if (fp8) {
+        if (head_dim == 128)
+            attention_small_kernel<128, true><<<grid, kDecWaves * 64, 0, s>>>(a, units);
+        else
+            attention_small_kernel<64, true><<<grid, kDecWaves * 64, 0, s>>>(a, units);
+    } else {
+        if (head_dim == 128)
+            attention_small_kernel<128, false><<<grid, kDecWaves * 64, 0, s>>>(a, units);
+        else
+            attention_small_kernel<64, false><<<grid, kDecWaves * 64, 0, s>>>(a, units);
+    }
     return hipGetLastError();
 }
 

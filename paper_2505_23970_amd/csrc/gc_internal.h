@@ -121,12 +121,13 @@ inline WorkspaceLayout workspace_layout(int batch, int64_t items, int64_t combin
 struct AppendArgs {
     const uint16_t* k_new;
     const uint16_t* v_new;
-    uint16_t* k_pool;
-    uint16_t* v_pool;
+    void* k_pool;        // bf16 elements, or E4M3 codes for 8-bit pools
+    void* v_pool;
     const int32_t* prefix_lens;
     const int32_t* cu_new_lens;
     const int32_t* block_tables;
     int32_t batch, total_tokens, num_kv_heads, num_blocks, max_blocks;
+    float k_inv, v_inv;  // 8-bit pools: fl32(1 / scale) of each pool
 };
 
 struct PlanArgs {
@@ -155,7 +156,8 @@ struct AttnArgs {
     const WorkItem* items;
     int32_t num_q_heads, num_kv_heads, group, tq;
     int32_t num_blocks, max_blocks;
-    float scale_log2;    // softmax scale * log2(e)
+    float scale_log2;    // softmax scale * log2(e) (times the key scale for 8-bit pools)
+    float v_scale;       // value scale of 8-bit pools, 1 for bf16 pools
 };
 
 struct CombineArgs {
@@ -170,10 +172,12 @@ struct CombineArgs {
     int32_t batch, num_partials, block_m;
 };
 
-hipError_t launch_append(const AppendArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, hipStream_t s);
-hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
+                            hipStream_t s);
+hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, bool fp8,
+                                  hipStream_t s);
 hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s);
 

@@ -86,8 +86,9 @@ def sample_rows(w: W.Workload, tokens_per_request=6, heads_per_kv=2, seed=0):
 
 
 def compare_attention(w: W.Workload, out_dev, lse_dev, ref_out, ref_lse, rows=None,
-                      contract=True):
-    """Compare GPU rows with oracle rows; returns a dict of error figures."""
+                      contract=True, vmax=None):
+    """Compare GPU rows with oracle rows; returns a dict of error figures. `vmax`
+    (largest value magnitude) defaults to that of the bf16 values of w."""
     T, Hq, D = w.q.shape
     got = from_dev_f32(out_dev).reshape(T * Hq, D)
     got_lse = from_dev_f32(lse_dev).reshape(T * Hq) if lse_dev is not None else None
@@ -96,8 +97,9 @@ def compare_attention(w: W.Workload, out_dev, lse_dev, ref_out, ref_lse, rows=No
         got_lse = got_lse[rows] if got_lse is not None else None
     assert not np.isnan(got).any(), "NaN in the output"
     err = np.abs(got - ref_out)
-    vmax = float(np.abs(W.bf16_bits_to_f32(np.concatenate(
-        [w.v_new.ravel(), w.v_prefix.ravel()]))).max(initial=0.0))
+    if vmax is None:
+        vmax = float(np.abs(W.bf16_bits_to_f32(np.concatenate(
+            [w.v_new.ravel(), w.v_prefix.ravel()]))).max(initial=0.0))
     bound = derived_bound(ref_out, vmax)
     worst = np.unravel_index(np.argmax(err - bound), err.shape) if err.size else None
     info = {"max_abs": float(err.max(initial=0.0)), "mean_abs": float(err.mean()) if err.size else 0.0,
@@ -124,3 +126,63 @@ def oracle_pools(w: W.Workload):
 def oracle_rows(w: W.Workload, kp, vp, rows=None):
     return oracle.attention(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q, kp, vp,
                             w.scale, rows=rows)
+
+
+# ----------------------------------------------------------------- 8-bit pools
+
+def to_dev_u8(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, np.uint8)).to("cuda")
+
+
+class DeviceRunFp8:
+    """HIP path over 8-bit pools: the initial pools come from W.e4m3_pools(w)."""
+
+    def __init__(self, w: W.Workload, k_scale, v_scale):
+        import paper_2505_23970_amd as gc
+        self.w, self.ks, self.vs = w, k_scale, v_scale
+        self.batch = gc.PagedBatch(w.prefix_lens, w.new_lens, w.block_tables)
+        self.k8_init, self.v8_init = W.e4m3_pools(w)
+        self.q = to_dev_bf16(w.q)
+        self.k_new = to_dev_bf16(w.k_new)
+        self.v_new = to_dev_bf16(w.v_new)
+        self.k_pool = to_dev_u8(self.k8_init)
+        self.v_pool = to_dev_u8(self.v8_init)
+
+    def append(self):
+        import paper_2505_23970_amd as gc
+        gc.kv_append_fp8(self.k_new, self.v_new, self.k_pool, self.v_pool, self.batch, self.ks, self.vs)
+
+    def pools(self):
+        return self.k_pool.cpu().numpy(), self.v_pool.cpu().numpy()
+
+    def attention(self, kv_split_tiles=None, tiling=None):
+        import torch
+        import paper_2505_23970_amd as gc
+        T, Hq, D = self.w.q.shape
+        lse = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+        out = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+        gc.prefix_prefill_attention_fp8(self.q, self.k_pool, self.v_pool, self.batch, self.w.scale,
+                                        self.ks, self.vs, out=out, lse=lse,
+                                        kv_split_tiles=kv_split_tiles, tiling=tiling)
+        torch.cuda.synchronize()
+        return out, lse
+
+
+def oracle_pools_fp8(run: DeviceRunFp8):
+    w = run.w
+    return oracle.kv_append_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                 w.k_new, w.v_new, run.k8_init, run.v8_init, run.ks, run.vs)
+
+
+def oracle_rows_fp8(run: DeviceRunFp8, kp8, vp8, rows=None):
+    w = run.w
+    return oracle.attention_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q,
+                                 kp8, vp8, run.ks, run.vs, w.scale, rows=rows)
+
+
+def e4m3_vmax(codes, scale):
+    """Largest finite dequantised magnitude among `codes`."""
+    table = np.array([abs(oracle.e4m3_value(c)) for c in range(256)], np.float64)
+    vals = table[np.unique(codes)]
+    return float(np.nanmax(vals)) * scale

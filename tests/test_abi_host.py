@@ -184,3 +184,30 @@ def test_split_grows_workspace(lib):
 def test_binding_refuses_missing_library(tmp_path):
     with pytest.raises(RuntimeError):
         gc.load_library(str(tmp_path / "nope.so"))
+
+
+def test_fp8_entry_points_check_scales_on_the_host(lib):
+    b = HostBatch([4], [3])
+    g = geo()
+    p = 0x2000
+
+    def app(ks, vs, ptrs=(p, p, p, p)):
+        kn, vn, kp, vp = ptrs
+        return lib.gc_kv_append_fp8(ctypes.byref(g), ctypes.byref(b.desc), kn, vn, ks, vs, kp, vp, None)
+
+    def run(ks, vs):
+        return lib.gc_prefix_prefill_run_fp8(ctypes.byref(g), ctypes.byref(b.desc),
+                                             ctypes.byref(NEVER_SPLIT), p, p, p, ks, vs, 0.125, p,
+                                             None, 0x3000, 1 << 40, None)
+
+    for ks, vs in ((0.0, 1.0), (1.0, -2.0), (float("nan"), 1.0), (1.0, float("inf")),
+                   (1e-45, 1.0)):  # the last one: fl32(1 / scale) overflows
+        assert app(ks, vs) == -2, (ks, vs)
+        assert run(ks, vs) == -2, (ks, vs)
+    assert app(0.5, 0.25, ptrs=(p, None, p, p)) == -1
+    assert lib.gc_prefix_prefill_attention_fp8(ctypes.byref(g), ctypes.byref(b.desc), None, p, None, p,
+                                               0.5, 0.5, 0.125, p, None, 0x3000, 1 << 40, None) == -1
+    # an empty batch is a no-op even for 8-bit pools
+    e = HostBatch([], [], fake_dev=False)
+    assert lib.gc_kv_append_fp8(ctypes.byref(g), ctypes.byref(e.desc), None, None, 0.5, 0.5, None,
+                                None, None) == 0

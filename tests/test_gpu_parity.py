@@ -355,3 +355,77 @@ def test_restore_refuses_pageable_host_memory():
     ks = torch.from_numpy(w.k_prefix.view(np.int16)).view(torch.bfloat16)
     with pytest.raises(ValueError):
         gc.kv_restore(ks, ks, run.k_pool, run.v_pool, run.batch)
+
+
+# ----------------------------------------------------------------- 8-bit (E4M3) pools
+
+E4M3_NAN_CODES = (0x7F, 0xFF)
+
+
+@pytest.mark.parametrize("ks,vs", [(1.0, 1.0), (0.37, 0.0113), (2.0 ** -7, 3.1 / 448.0)])
+def test_fp8_append_quantises_every_bf16_value_like_the_oracle(ks, vs):
+    """Every bf16 bit pattern goes through the 8-bit append (keys in order, values
+    shuffled); codes must equal the oracle's bit for bit, except that a NaN input
+    may become either NaN code."""
+    w = W.build([5, 0], [200, 56], 4, 2, 128, seed=120, name="e4m3_all_bf16")
+    allbits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    w.k_new = allbits.reshape(256, 2, 128).copy()
+    w.v_new = np.random.default_rng(121).permutation(allbits).reshape(256, 2, 128)
+    say(f"case {w.name}: scales {ks} {vs}")
+    run = H.DeviceRunFp8(w, ks, vs)
+    run.append()
+    kp, vp = run.pools()
+    kref, vref = H.oracle_pools_fp8(run)
+    for got, ref, name in ((kp, kref, "k"), (vp, vref, "v")):
+        diff = got != ref
+        if diff.any():
+            assert np.isin(got[diff], E4M3_NAN_CODES).all() and np.isin(ref[diff], E4M3_NAN_CODES).all(), (
+                f"{name}_pool differs at {np.argwhere(diff)[:5]}: got {got[diff][:5]}, ref {ref[diff][:5]}")
+        n_nan_inputs = int(np.isnan(W.bf16_bits_to_f32(allbits)).sum())
+        assert int(diff.sum()) <= n_nan_inputs
+
+
+def fp8_check(w, ks, vs, kv_split_tiles=None, tiling=None, rows=None, contract=True):
+    say(f"case {w.name} (8-bit pools, scales {ks} {vs}): B={w.batch} Hq={w.num_q_heads} "
+        f"Hkv={w.num_kv_heads} D={w.head_dim} T={w.total_new} split={kv_split_tiles} tiling={tiling}")
+    run = H.DeviceRunFp8(w, ks, vs)
+    run.append()
+    kref, vref = H.oracle_pools_fp8(run)
+    kp, vp = run.pools()
+    assert np.array_equal(kp, kref), f"k_pool differs at {np.argwhere(kp != kref)[:5]}"
+    assert np.array_equal(vp, vref), f"v_pool differs at {np.argwhere(vp != vref)[:5]}"
+    out, lse = run.attention(kv_split_tiles=kv_split_tiles, tiling=tiling)
+    ref_out, ref_lse = H.oracle_rows_fp8(run, kref, vref, rows=rows)
+    vmax = H.e4m3_vmax(vref, vs)
+    return H.compare_attention(w, out, lse, ref_out, ref_lse, rows=rows, contract=contract, vmax=vmax)
+
+
+@pytest.mark.parametrize("split", [None, 2])
+@pytest.mark.parametrize("tiling", ["prefill", "wide", "small"])
+def test_fp8_pools_every_tiling(tiling, split):
+    import paper_2505_23970_amd as gc
+    t = {"prefill": gc.TILES_PREFILL, "wide": gc.TILES_WIDE, "small": gc.TILES_SMALL}[tiling]
+    w = W.build(seed=110, name=f"fp8_{tiling}", **SUITE_SHAPE)
+    info = fp8_check(w, 0.0113, 0.0271, kv_split_tiles=split, tiling=t)
+    say(f"8-bit {tiling} split {split}: {info}")
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_fp8_pools_ragged_edges(D):
+    """Empty suffixes and prefixes, one-token requests and page-straddling lengths,
+    automatic tiling."""
+    w = W.build([0, 17, 1, 250, 0], [33, 1, 70, 0, 5], 8, 2, D, seed=111, name=f"fp8_edges_d{D}")
+    info = fp8_check(w, 0.02, 0.015)
+    say(f"8-bit edges D={D}: {info}")
+
+
+def test_fp8_config2_all_rows():
+    w = W.make_config(2)
+    info = fp8_check(w, 2.0 ** -6, 0.0213)
+    say(f"8-bit config 2: {info}")
+
+
+def test_fp8_decode_workload_sampled():
+    w = W.decode_variant()
+    info = fp8_check(w, 2.0 ** -6, 0.0213, rows=H.sample_rows(w, seed=51))
+    say(f"8-bit decode, 32 requests: {info}")
