@@ -3,7 +3,9 @@
 
 One step = the whole hot path over one batch already resident in HBM:
 KV append of the new tokens (gc_kv_append), work-list planning
-(gc_prefix_prefill_plan) and attention (gc_prefix_prefill_run). The default
+(gc_prefix_prefill_plan) and attention (gc_prefix_prefill_run). With
+--kv fp8 the pools hold 8-bit E4M3 codes (gc_kv_append_fp8 and
+gc_prefix_prefill_run_fp8; products still bf16 x bf16 -> fp32). The default
 workload is the Llama-3-8B attention shape (32 query / 8 KV heads, head_dim
 128, 8 ragged requests with cached prefixes of 1024-4096 tokens and 64-512
 new tokens, page 16, random block permutation), drawn from a fixed seed.
@@ -66,6 +68,8 @@ def parse():
     # default warm-up is long enough to time the steady state of a serving loop.
     ap.add_argument("--warmup", type=int, default=400)
     ap.add_argument("--workload", default="llama3_8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--kv", default="bf16", choices=["bf16", "fp8"],
+                    help="KV pool element type: bf16, or 8-bit E4M3 codes with one scale per pool")
     ap.add_argument("--kv-split-tiles", type=int, default=None,
                     help="override the automatic split policy (0 auto, <0 never, >0 tiles)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -141,6 +145,29 @@ def restore_benchmark(w, steps, warmup):
     print(json.dumps(rec), flush=True)
 
 
+# Pool scales of the 8-bit runs (the pool generator's codes have magnitudes 2^-5 .. 15).
+K_SCALE_FP8 = 2.0 ** -6
+V_SCALE_FP8 = 0.0213
+
+
+def auto_kernel_name(w, cus, fp8):
+    """Kernel the library's automatic tiling picks for w (the rule of choose_tiling in
+    the C ABI, restated: small tiles when every request has n * g <= 16, else wide
+    tiles when 256-row tiles are >= 85 % full and their grid is not between one and
+    two per compute unit, else 128-row tiles)."""
+    g = w.num_q_heads // w.num_kv_heads
+    D = w.head_dim
+    f = ", fp8" if fp8 else ""
+    if g <= 16 and int(w.new_lens.max()) * g <= 16:
+        return f"attention_small_kernel<{D}{f}> (+ split merge when the plan splits)"
+    tq = 256 // g
+    units = int(sum((int(n) + tq - 1) // tq for n in w.new_lens))
+    rows = int(w.new_lens.sum()) * g
+    grid = units * w.num_kv_heads
+    wide = rows * 100 >= units * 256 * 85 and not (cus < grid < 2 * cus)
+    return f"attention_kernel<{D}, {8 if wide else 4}{f}> (+ split merge when the plan splits)"
+
+
 def measured_read_gbs(mib=4096, reps=5):
     """Sustained HBM read rate on this GPU: the library's streaming-read probe over
     a 4 GiB buffer, timed with HIP events. The nominal 8 TB/s is not reachable by
@@ -184,11 +211,17 @@ def profiled_traffic(workload):
     return rec["traffic_bytes"] if rec.get("kernel_source_sha256_16") == sha else None
 
 
-def cpu_oracle_baseline(w, target_s):
-    """Time the fp64 oracle on a bounded sample of the workload's output rows."""
+def cpu_oracle_baseline(w, target_s, fp8=None):
+    """Time the fp64 oracle on a bounded sample of the workload's output rows.
+    fp8 = (k_pool8, v_pool8, k_scale, v_scale) times the 8-bit-pool oracle."""
     import oracle
-    kp, vp = oracle.kv_append(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
-                              w.k_new, w.v_new, w.k_pool, w.v_pool)
+    if fp8 is None:
+        kp, vp = oracle.kv_append(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                  w.k_new, w.v_new, w.k_pool, w.v_pool)
+    else:
+        k8, v8, ks, vs = fp8
+        kp, vp = oracle.kv_append_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks,
+                                       w.k_new, w.v_new, k8, v8, ks, vs)
     T, Hq, D = w.q.shape
     cu = w.cu_new_lens
     req = np.repeat(np.arange(w.batch), w.new_lens)
@@ -200,8 +233,12 @@ def cpu_oracle_baseline(w, target_s):
 
     def timed(rows):
         t0 = time.perf_counter()
-        oracle.attention(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q, kp, vp,
-                         w.scale, rows=rows)
+        if fp8 is None:
+            oracle.attention(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q, kp, vp,
+                             w.scale, rows=rows)
+        else:
+            oracle.attention_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, w.q, kp,
+                                  vp, fp8[2], fp8[3], w.scale, rows=rows)
         return time.perf_counter() - t0
 
     # calibrate on a small slice, then size the sample to about target_s seconds
@@ -213,7 +250,7 @@ def cpu_oracle_baseline(w, target_s):
     t = timed(rows)
     flops = float(np.sum(4.0 * D * keys_per_token[rows // Hq]))
     sample = (f"{n_rows} of {T * Hq} output rows (token, query head) drawn uniformly at random; "
-              f"fp64 oracle, append excluded")
+              f"fp64 oracle{' over 8-bit pools' if fp8 is not None else ''}, append excluded")
     return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": sample, "seconds": t,
             "new_tokens_per_s_equiv": (n_rows / Hq) / t}
@@ -243,9 +280,16 @@ def main():
     def up(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
 
+    fp8 = args.kv == "fp8"
     batch = gc.PagedBatch(w.prefix_lens, w.new_lens, w.block_tables, device=dev)
     q, k_new, v_new = up(w.q), up(w.k_new), up(w.v_new)
-    k_pool, v_pool = up(w.k_pool), up(w.v_pool)
+    if fp8:
+        from paper_2505_23970_amd import workloads as W
+        k8, v8 = W.e4m3_pools(w)
+        k_pool = torch.from_numpy(k8).to(dev)
+        v_pool = torch.from_numpy(v8).to(dev)
+    else:
+        k_pool, v_pool = up(w.k_pool), up(w.v_pool)
     out = torch.empty_like(q)
     ws = gc.alloc_workspace(Hq, k_pool, v_pool, batch, args.kv_split_tiles)
     torch.cuda.synchronize()
@@ -253,13 +297,20 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        gc.kv_append(k_new, v_new, k_pool, v_pool, batch)
+        if fp8:
+            gc.kv_append_fp8(k_new, v_new, k_pool, v_pool, batch, K_SCALE_FP8, V_SCALE_FP8)
+        else:
+            gc.kv_append(k_new, v_new, k_pool, v_pool, batch)
         if ev is not None:
             ev[1].record()
         gc.plan(Hq, k_pool, v_pool, batch, ws, args.kv_split_tiles)
         if ev is not None:
             ev[2].record()
-        gc.run(q, k_pool, v_pool, batch, w.scale, ws, out=out, kv_split_tiles=args.kv_split_tiles)
+        if fp8:
+            gc.run_fp8(q, k_pool, v_pool, batch, w.scale, K_SCALE_FP8, V_SCALE_FP8, ws, out=out,
+                       kv_split_tiles=args.kv_split_tiles)
+        else:
+            gc.run(q, k_pool, v_pool, batch, w.scale, ws, out=out, kv_split_tiles=args.kv_split_tiles)
         if ev is not None:
             ev[3].record()
 
@@ -282,15 +333,13 @@ def main():
     t_att = float(np.mean(att)) * 1e-3
 
     achieved = F / t_att / 1e12
-    g = w.num_q_heads // w.num_kv_heads
-    small = g <= 16 and int(w.new_lens.max()) * g <= 16  # the library's automatic tiling rule
-    kernel_name = (("attention_small_kernel" if small else "attention_kernel") + f"<{D}>"
-                   + " (+ split merge when the plan splits)")
+    kernel_name = auto_kernel_name(w, torch.cuda.get_device_properties(0).multi_processor_count, fp8)
+    A = w.attn_bytes(1 if fp8 else 2)
     # the binding roof follows the workload's arithmetic intensity (flop per algorithmic byte)
     ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
-    hbm_bound = F / w.attn_bytes() < ridge
+    hbm_bound = F / A < ridge
     if hbm_bound:
-        roof = {"bound": "hbm", "achieved": w.attn_bytes() / t_att / 1e9, "peak": PEAK_HBM_GBS,
+        roof = {"bound": "hbm", "achieved": A / t_att / 1e9, "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     else:
         roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
@@ -313,23 +362,26 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, **{k: v for k, v in w.describe().items() if k != "workload"},
-                   "kv_split_tiles": args.kv_split_tiles},
+                   "kv_split_tiles": args.kv_split_tiles,
+                   "kv_pool": ({"type": "e4m3", "k_scale": K_SCALE_FP8, "v_scale": V_SCALE_FP8}
+                               if fp8 else {"type": "bf16"})},
         "new_tokens_per_s": T / (ms_step * 1e-3),
         "attention_tflops": achieved,
         "kernel_ms": {"append": float(np.mean(app)), "plan": float(np.mean(pln)),
                       "attention": float(np.mean(att)),
                       "attention_p10": float(np.percentile(att, 10)),
                       "attention_p90": float(np.percentile(att, 90))},
-        "algorithmic": {"flops": F, "attn_bytes": w.attn_bytes(), "append_bytes": w.append_bytes()},
+        "algorithmic": {"flops": F, "attn_bytes": A, "append_bytes": w.append_bytes()},
         "roofline": {**roof,
-                     "traffic": profiled_traffic(w.name),
+                     "traffic": profiled_traffic(w.name + ("_fp8" if fp8 else "")),
                      "kernel": kernel_name,
-                     "arithmetic_intensity": F / w.attn_bytes(),
+                     "arithmetic_intensity": F / A,
                      "mfma_frac": achieved / PEAK_BF16_TFLOPS,
-                     "hbm_gbs_algorithmic": w.attn_bytes() / t_att / 1e9},
+                     "hbm_gbs_algorithmic": A / t_att / 1e9},
     }
     if args.cpu_seconds > 0:
-        rec["cpu_baseline"] = cpu_oracle_baseline(w, args.cpu_seconds)
+        rec["cpu_baseline"] = cpu_oracle_baseline(
+            w, args.cpu_seconds, (k8, v8, K_SCALE_FP8, V_SCALE_FP8) if fp8 else None)
     else:
         rec["cpu_baseline"] = None
     print(json.dumps(rec), flush=True)

@@ -103,13 +103,14 @@ class Workload:
         pairs = float(np.sum(n * P + n * (n + 1) / 2))
         return 4.0 * self.head_dim * self.num_q_heads * pairs
 
-    def attn_bytes(self) -> float:
+    def attn_bytes(self, kv_elem_bytes: int = 2) -> float:
         """Algorithmic HBM bytes of the attention kernel: K and V of every key read
-        once per KV head, Q read once and O written once (bf16)."""
+        once per KV head (kv_elem_bytes per element: 2 for bf16 pools, 1 for 8-bit
+        pools), Q read once and O written once (bf16)."""
         L = (self.prefix_lens + self.new_lens).astype(np.float64)
         n = self.new_lens.astype(np.float64)
         D, Hq, Hkv = self.head_dim, self.num_q_heads, self.num_kv_heads
-        return float(np.sum(4.0 * Hkv * D * L + 4.0 * Hq * D * n))
+        return float(np.sum(2.0 * kv_elem_bytes * Hkv * D * L + 4.0 * Hq * D * n))
 
     def append_bytes(self) -> float:
         """Algorithmic bytes of the KV append: read new K/V, write them into the pool."""
