@@ -1,7 +1,8 @@
-"""Build libgreencache.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Build libgreencache.so (the HIP kernels and the C ABI) for gfx950 with hipcc,
+and libgreencache_ctl.so (the CPU replacement model) with g++.
 
-Run as `python -m paper_2505_23970_amd.build`; writes the library next to
-this file so that it travels with the source tree.
+Run as `python -m paper_2505_23970_amd.build`; writes the libraries next to
+this file so that they travel with the source tree.
 """
 from __future__ import annotations
 
@@ -24,8 +25,25 @@ HIPCC_FLAGS = [
 ]
 
 
+CONTROL_LIBRARY = os.path.join(HERE, "libgreencache_ctl.so")
+# IEEE double without contraction: the replacement scores are compared exactly
+CONTROL_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden", "-ffp-contract=off",
+                 "-Wall", "-Wextra"]
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+
+
+def build_control(out: str = CONTROL_LIBRARY) -> str:
+    tmp = out + f".tmp{os.getpid()}"
+    cmd = ["g++", *CONTROL_FLAGS, "-I", os.path.join(ROOT, "include"),
+           os.path.join(CSRC, "cache_policy.cpp"), "-o", tmp]
+    res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"g++ failed ({res.returncode}):\n{res.stdout}")
+    os.replace(tmp, out)
+    return out
 
 
 def build(out: str = LIBRARY, extra=(), verbose=False) -> str:
@@ -49,3 +67,4 @@ def build(out: str = LIBRARY, extra=(), verbose=False) -> str:
 
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    print(build_control())

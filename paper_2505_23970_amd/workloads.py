@@ -358,3 +358,107 @@ def set_position_code(w: Workload) -> Workload:
             arr, idx = _logical_v(w, r, j)
             arr[idx, :, 0] = f32_to_bf16_bits(np.float32(j))
     return w.finish()
+
+
+# ----------------------------------------------------------------- request traces (control plane)
+# Synthetic stand-ins for the paper's ShareGPT multi-turn chats and TriviaQA
+# document questions (§6.1), which are not available. Each request is
+# (key, context_tokens, prompt_tokens, total_tokens, turn, time) as the cache
+# model of include/greencache_ctl.h defines them.
+
+TRACE_DTYPE = np.dtype([("key", "<i8"), ("context_tokens", "<i8"), ("prompt_tokens", "<i8"),
+                        ("total_tokens", "<i8"), ("turn", "<i4"), ("reserved", "<i4"), ("time", "<f8")])
+
+# KV bytes per token of Llama-3-70B (80 layers, 8 KV heads, head_dim 128, K and V, bf16)
+LLAMA3_70B_KV_BYTES_PER_TOKEN = 2 * 80 * 8 * 128 * 2
+
+
+def _lognormal_int(rng, median, sigma, lo, hi, size):
+    return np.clip(np.rint(median * np.exp(sigma * rng.standard_normal(size))), lo, hi).astype(np.int64)
+
+
+def chat_trace(seed: int = SEED_BASE + 60, hours: float = 24.0, sessions_per_s: float = 0.4,
+               mean_turns: float = 4.0, window: int = 8192, think_s: float = 3600.0) -> np.ndarray:
+    """Multi-turn conversations: sessions arrive as a Poisson process; each has
+    1 + Geometric turns (mean `mean_turns`); a turn adds a user prompt (lognormal,
+    median 60 tokens) and a response (median 200 tokens); think time between turns
+    is exponential with mean `think_s` (1 h: the conversations of a day-long trace
+    are resumed later, not answered back to back). Turn k's context is everything before it; a
+    session ends once its context would exceed the model's `window` (8k, §6.1)."""
+    rng = np.random.default_rng(seed)
+    horizon = hours * 3600.0
+    n_sessions = int(rng.poisson(sessions_per_s * horizon))
+    starts = np.sort(rng.uniform(0.0, horizon, n_sessions))
+    rows = []
+    for sid, t0 in enumerate(starts):
+        turns = int(rng.geometric(1.0 / mean_turns))  # >= 1, mean `mean_turns`
+        user = _lognormal_int(rng, 60, 1.0, 4, 2048, turns)
+        resp = _lognormal_int(rng, 200, 0.8, 8, 2048, turns)
+        gaps = rng.exponential(think_s, turns)
+        ctx, t = 0, float(t0)
+        for k in range(turns):
+            prompt = ctx + int(user[k])
+            total = prompt + int(resp[k])
+            if total > window or t >= horizon:
+                break
+            rows.append((sid, ctx, prompt, total, k + 1, 0, t))
+            ctx = total
+            t += float(gaps[k])
+    tr = np.array(rows, dtype=TRACE_DTYPE)
+    return tr[np.argsort(tr["time"], kind="stable")]
+
+
+def document_trace(seed: int = SEED_BASE + 61, hours: float = 24.0, questions_per_s: float = 1.5,
+                   documents: int = 20000, alpha: float = 0.7, window: int = 8192) -> np.ndarray:
+    """Document questions: `documents` documents with lognormal lengths (median
+    4000 tokens, clipped to the 8k window); questions arrive as a Poisson process
+    and pick a document with Zipf(alpha) popularity (the paper's alpha 0.4 and
+    0.7, §6.5); the cached entry is the document (context = document length),
+    the question (median 20 tokens) is not reused."""
+    rng = np.random.default_rng(seed)
+    horizon = hours * 3600.0
+    lengths = _lognormal_int(rng, 4000, 0.5, 500, window - 64, documents)
+    p = 1.0 / np.arange(1, documents + 1, dtype=np.float64) ** alpha
+    p /= p.sum()
+    n = int(rng.poisson(questions_per_s * horizon))
+    times = np.sort(rng.uniform(0.0, horizon, n))
+    docs = rng.choice(documents, size=n, p=p)
+    q = _lognormal_int(rng, 20, 0.5, 4, 64, n)
+    turn = np.zeros(documents, np.int64)
+    tr = np.zeros(n, dtype=TRACE_DTYPE)
+    for i in range(n):
+        d = int(docs[i])
+        turn[d] += 1
+        tr[i] = (d, lengths[d], lengths[d] + q[i], lengths[d] + q[i], turn[d], 0, times[i])
+    return tr
+
+
+def ilp_profile(seed: int = SEED_BASE + 62, steps: int = 24, sizes_tb=tuple(range(17)),
+                slo_ttft_s: float = 2.5):
+    """A synthetic profile for the cache-size ILP (§5.2-5.4): per hour t, a
+    request count (diurnal) and a grid carbon intensity (diurnal, gCO2e/kWh); per
+    (t, size) a mean TTFT that falls with the cache's token hit rate (which grows
+    with size and saturates) and rises with load, a mean power, and the numbers
+    of requests meeting the TTFT and TPOT SLOs (2.5 s / 0.2 s for the 70B chat
+    task, §6.1). Returns a dict of numpy arrays."""
+    rng = np.random.default_rng(seed)
+    t = np.arange(steps)
+    rate = 1.0 + 0.8 * np.sin(2 * np.pi * (t - 8) / 24.0) + 0.1 * rng.standard_normal(steps)
+    rate = np.clip(rate, 0.2, None)                                   # requests/s
+    n = np.rint(rate * 3600.0).astype(np.int64)
+    ci = 120.0 + 80.0 * np.cos(2 * np.pi * (t - 13) / 24.0) + 10 * rng.standard_normal(steps)
+    ci = np.clip(ci, 20.0, None)
+    S = np.asarray(sizes_tb, np.float64)
+    hit = 0.7 * (1.0 - np.exp(-S / 6.0))                             # token hit rate vs size
+    load = rate[:, None] / 1.8
+    ttft = (1.2 + 2.0 * load ** 2) * (1.0 - 0.8 * hit[None, :])      # seconds
+    tpot = 0.12 + 0.1 * load * (1.0 - 0.5 * hit[None, :])
+    power = 1200.0 + 400.0 * load * (1.0 - 0.3 * hit[None, :])        # watts
+    spread_ttft = 0.35 * ttft
+    z_ttft = (slo_ttft_s - ttft) / spread_ttft
+    z_tpot = (0.2 - tpot) / (0.25 * tpot)
+    from math import erf
+    cdf = np.vectorize(lambda z: 0.5 * (1.0 + erf(z / np.sqrt(2.0))))
+    ok_ttft = np.rint(n[:, None] * cdf(z_ttft)).astype(np.int64)
+    ok_tpot = np.rint(n[:, None] * cdf(z_tpot)).astype(np.int64)
+    return dict(n=n, ci=ci, sizes_tb=S, ttft=ttft, power=power, ok_ttft=ok_ttft, ok_tpot=ok_tpot)

@@ -1,0 +1,158 @@
+"""The control plane's product code (native replacement model, carbon model, ILP
+solver) against the control oracle (CPU only)."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import control as O
+from paper_2505_23970_amd import control as K
+from paper_2505_23970_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "greencache_ctl.h")
+POL = {"fifo": O.FIFO, "lru": O.LRU, "lcs": O.LCS, "lcs_multiturn": O.LCS_MULTITURN}
+
+
+def test_header_declares_the_binding_surface():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    assert sorted(set(re.findall(r"\b(gc_cache_\w+)\s*\(", text))) == sorted(K.EXPORTED)
+    lib = K.load_library()
+    for name in K.EXPORTED:
+        assert hasattr(lib, name)
+
+
+def test_bad_arguments_change_nothing():
+    lib = K.load_library()
+    h = ctypes.c_void_p()
+    assert lib.gc_cache_create(7, 100, 1, ctypes.byref(h)) == -2
+    assert lib.gc_cache_create(0, -1, 1, ctypes.byref(h)) == -2
+    assert lib.gc_cache_create(0, 100, 0, ctypes.byref(h)) == -2
+    assert lib.gc_cache_create(0, 100, 1, None) == -1
+    c = K.Cache("lru", 100, 1)
+    ok = np.zeros(2, K.REQUEST_DTYPE)
+    ok[:] = [(1, 0, 5, 10, 1, 0, 0.0), (2, 0, 5, 10, 1, 0, 1.0)]
+    c.replay(ok)
+    before = c.stats()
+    for field, value in (("prompt_tokens", 1), ("total_tokens", 4), ("reserved", 1), ("time", 0.5),
+                         ("time", float("nan")), ("context_tokens", -1)):
+        bad = np.zeros(2, K.REQUEST_DTYPE)
+        bad[:] = [(3, 0, 5, 10, 1, 0, 2.0), (4, 2, 5, 10, 1, 0, 3.0)]
+        bad[1][field] = value
+        with pytest.raises(K.CtlError):
+            c.replay(bad)
+        assert c.stats() == before, field
+    with pytest.raises(K.CtlError):
+        c.resize(10, 0.5)  # time going backwards
+    assert c.stats() == before
+
+
+def small_traces():
+    chat = W.chat_trace(seed=7, hours=3.0, sessions_per_s=0.05, think_s=600.0)
+    doc = W.document_trace(seed=8, hours=1.0, questions_per_s=0.5, documents=300, alpha=0.7)
+    return {"chat": chat, "doc": doc}
+
+
+@pytest.mark.parametrize("policy", sorted(POL))
+@pytest.mark.parametrize("trace", ["chat", "doc"])
+def test_replay_matches_the_oracle_decision_for_decision(policy, trace):
+    tr = small_traces()[trace]
+    rows = [(int(r["key"]), int(r["context_tokens"]), int(r["prompt_tokens"]), int(r["total_tokens"]),
+             int(r["turn"]), float(r["time"])) for r in tr]
+    unique = int(np.sum(tr["total_tokens"] - tr["context_tokens"]))
+    for frac in (0.05, 0.2, 0.6):
+        cap = int(unique * frac)
+        c = K.Cache(policy, cap, 1)
+        got = c.replay(tr)
+        want, oc = O.replay(POL[policy], cap, 1, rows)
+        assert np.array_equal(got, np.array(want, np.int64)), (policy, trace, frac)
+        assert list(c.keys()) == sorted(oc.entries)
+        st = c.stats()
+        assert (st["hits"], st["reused_tokens"], st["insertions"], st["evictions"], st["bytes"]) == \
+            (oc.hits, oc.reused, oc.insertions, oc.evictions, oc.bytes())
+
+
+@pytest.mark.parametrize("policy", sorted(POL))
+def test_resize_matches_the_oracle(policy):
+    tr = small_traces()["doc"]
+    rows = [(int(r["key"]), int(r["context_tokens"]), int(r["prompt_tokens"]), int(r["total_tokens"]),
+             int(r["turn"]), float(r["time"])) for r in tr]
+    half = len(tr) // 2
+    cap = int(np.sum(tr["total_tokens"] - tr["context_tokens"]) * 0.4)
+    c = K.Cache(policy, cap, 1)
+    oc = O.Cache(POL[policy], cap, 1)
+    c.replay(tr[:half])
+    for r in rows[:half]:
+        oc.access(*r)
+    t = float(tr[half - 1]["time"])
+    c.resize(cap // 3, t)
+    oc.resize(cap // 3, t)
+    assert list(c.keys()) == sorted(oc.entries)
+    got = c.replay(tr[half:])
+    want = [oc.access(*r) for r in rows[half:]]
+    assert np.array_equal(got, np.array(want, np.int64))
+
+
+def test_hand_worked_cases_through_the_library():
+    import json
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "lcs_example.json")))
+    for case in g["cases"]:
+        tr = np.zeros(len(case["requests"]), K.REQUEST_DTYPE)
+        tr[:] = [(q["key"], q["context"], q["prompt"], q["total"], q["turn"], 0, q["time"])
+                 for q in case["requests"]]
+        c = K.Cache(case["policy"], case["capacity"], 1)
+        reused = c.replay(tr)
+        if "resize" in case:
+            c.resize(case["resize"]["capacity"], case["resize"]["time"])
+        if "expected_reused" in case:
+            assert list(reused) == case["expected_reused"], case["name"]
+        assert list(c.keys()) == case["expected_keys_after"], case["name"]
+
+
+def test_carbon_model_matches_the_oracle():
+    rng = np.random.default_rng(9)
+    p = K.Platform()
+    for _ in range(50):
+        power, ttft, ci, size = rng.uniform(100, 3000), rng.uniform(0.05, 20), rng.uniform(0, 700), int(rng.integers(0, 17))
+        got = float(K.request_carbon_g(power, ttft, ci, size, p))
+        want = O.request_carbon_g(power, ttft, ci, size, p.ssd_kg_per_tb, p.ssd_lifetime_years, p.others())
+        assert math.isclose(got, want, rel_tol=1e-12, abs_tol=1e-15)
+        e, h = rng.uniform(0, 50), rng.uniform(0, 24)
+        got = float(K.interval_carbon_g(e, ci, h, size, p))
+        want = O.total_g(e, ci, h, size, p.ssd_kg_per_tb, p.ssd_lifetime_years, p.others())
+        assert math.isclose(got, want, rel_tol=1e-12, abs_tol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_ilp_solver_matches_bruteforce(seed):
+    rng = np.random.default_rng(100 + seed)
+    T, S = int(rng.integers(2, 5)), int(rng.integers(2, 6))
+    n = rng.integers(5, 40, T)
+    cost = rng.uniform(1, 100, (T, S))
+    ok1 = np.minimum(n[:, None], rng.integers(0, 45, (T, S)))
+    ok2 = np.minimum(n[:, None], rng.integers(0, 45, (T, S)))
+    rho = float(rng.uniform(0.3, 0.95))
+    N = int(n.sum())
+    best, choice = K.solve_cache_sizes(cost, ok1, ok2, N, rho)
+    want, wchoice = O.solve_sizes_bruteforce(cost.tolist(), ok1.tolist(), ok2.tolist(), N, rho)
+    if want == math.inf:
+        assert best == math.inf and choice is None
+    else:
+        assert math.isclose(best, want, rel_tol=1e-9)
+        assert sum(ok1[t, s] for t, s in enumerate(choice)) >= rho * N - 1e-9
+        assert sum(ok2[t, s] for t, s in enumerate(choice)) >= rho * N - 1e-9
+
+
+def test_ilp_profile_costs_follow_the_per_request_term():
+    prof = W.ilp_profile(steps=3)
+    cost = K.profile_costs(prof)
+    p = K.Platform()
+    for t in range(3):
+        for s in (0, 5, 16):
+            want = prof["n"][t] * O.request_carbon_g(prof["power"][t, s], prof["ttft"][t, s], prof["ci"][t],
+                                                      prof["sizes_tb"][s], p.ssd_kg_per_tb,
+                                                      p.ssd_lifetime_years, p.others())
+            assert math.isclose(cost[t, s], want, rel_tol=1e-12)
