@@ -77,6 +77,8 @@ def parse():
     ap.add_argument("--restore", action="store_true",
                     help="instead of the benchmark, time restoring the workload's cached prefixes "
                          "from pinned host memory into the pool (the cache's host tier, over PCIe)")
+    ap.add_argument("--control", action="store_true",
+                    help="benchmark the CPU control plane instead (replacement model, ILP); no GPU")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead of the benchmark, run 5 plain device-to-device copies of this "
                          "many MiB (reference point that scales hardware byte counters)")
@@ -256,8 +258,76 @@ def cpu_oracle_baseline(w, target_s, fp8=None):
             "new_tokens_per_s_equiv": (n_rows / Hq) / t}
 
 
+def control_benchmark(cpu_seconds):
+    """The cache's control plane on synthetic day-long traces (§6.5 replacement
+    comparison, §5.4 ILP): token hit rates by policy and size, replay throughput
+    of the native replacement model, and the hourly cache-size decision."""
+    from paper_2505_23970_amd import control as K
+    from paper_2505_23970_amd import workloads as W
+    bpt = W.LLAMA3_70B_KV_BYTES_PER_TOKEN
+    traces = {"chat": W.chat_trace(), "doc_alpha0.4": W.document_trace(alpha=0.4),
+              "doc_alpha0.7": W.document_trace(alpha=0.7)}
+    sizes = (1, 2, 4, 8, 16)
+    table = {}
+    for name, tr in traces.items():
+        pols = ("fifo", "lru", "lcs", "lcs_multiturn") if name == "chat" else ("fifo", "lru", "lcs")
+        table[name] = {p: {str(tb): round(K.token_hit_rate(p, tb * 10**12, bpt, tr), 4) for tb in sizes}
+                       for p in pols}
+    tr = traces["chat"]
+    t0 = time.perf_counter()
+    c = K.Cache("lcs", 4 * 10**12, bpt)
+    c.replay(tr)
+    dt = time.perf_counter() - t0
+    value = len(tr) / dt
+    base = W.ilp_profile()
+    N = int(base["n"].sum())
+    ilp = {"steps": int(len(base["n"])), "sizes_tb": [int(x) for x in base["sizes_tb"]], "rho": 0.9}
+    # the synthetic grid's intensity as drawn, and scaled to a quarter (a low-carbon grid)
+    for attribution, ci_scale in (("ttft", 1.0), ("interval", 1.0), ("interval", 0.25)):
+        prof = dict(base, ci=base["ci"] * ci_scale)
+        cost = K.profile_costs(prof, cache_attribution=attribution)
+        t0 = time.perf_counter()
+        best, choice = K.solve_cache_sizes(cost, prof["ok_ttft"], prof["ok_tpot"], N, 0.9)
+        t_ilp = time.perf_counter() - t0
+
+        def fixed(s):
+            ok = (prof["ok_ttft"][:, s].sum() >= 0.9 * N) and (prof["ok_tpot"][:, s].sum() >= 0.9 * N)
+            return float(cost[:, s].sum()), bool(ok)
+        full_g, full_ok = fixed(len(prof["sizes_tb"]) - 1)
+        none_g, none_ok = fixed(0)
+        ilp[f"{attribution}_ci_x{ci_scale:g}"] = {"solve_s": t_ilp,
+                            "choice_tb": [int(prof["sizes_tb"][s]) for s in choice] if choice else None,
+                            "carbon_g": best, "full_cache_g": full_g, "full_cache_meets_slo": full_ok,
+                            "no_cache_g": none_g, "no_cache_meets_slo": none_ok}
+    rec = {
+        "metric": "control plane: replacement-model requests/s (LCS, 4 TB, chat trace); token hit rates; ILP",
+        "value": value, "unit": "requests/s", "n_gpus": 0, "higher_is_better": True,
+        "data": "synthetic", "config": {"workload": "chat_trace 24 h (Llama-3-70B KV, 320 KiB/token)",
+                                        "requests": int(len(tr)), "policy": "lcs", "capacity_tb": 4},
+        "token_hit_rate": table,
+        "ilp": ilp,
+    }
+    if cpu_seconds > 0:
+        import oracle.control as OC
+        rows = [(int(r["key"]), int(r["context_tokens"]), int(r["prompt_tokens"]), int(r["total_tokens"]),
+                 int(r["turn"]), float(r["time"])) for r in tr]
+        oc = OC.Cache(OC.LCS, 4 * 10**12, bpt)
+        t0 = time.perf_counter()
+        n = 0
+        while n < len(rows) and time.perf_counter() - t0 < cpu_seconds:
+            oc.access(*rows[n])
+            n += 1
+        dt = time.perf_counter() - t0
+        rec["cpu_baseline"] = {"value": n / dt, "unit": "requests/s", "cores": 1, "kind": "oracle",
+                               "sample": f"first {n} of {len(rows)} requests of the same trace and cache"}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse()
+    if args.control:
+        control_benchmark(args.cpu_seconds)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(this path has no multi-GPU mode)", file=sys.stderr)

@@ -167,12 +167,23 @@ def request_carbon_g(power_w, ttft_s, ci, size_tb, platform: Platform = Platform
 
 # ----------------------------------------------------------------- cache-size ILP
 
-def profile_costs(profile: dict, platform: Platform = Platform()) -> np.ndarray:
-    """cost[t, s] = requests of step t x the per-request carbon at cache size s."""
+def profile_costs(profile: dict, platform: Platform = Platform(), cache_attribution: str = "ttft",
+                  step_hours: float = 1.0) -> np.ndarray:
+    """cost[t, s] = requests of step t x the per-request carbon at cache size s.
+
+    cache_attribution "ttft" prices the SSD as Eq. 6 writes it (each request is
+    charged TTFT / LT_SSD x S x C_SSD,unit); "interval" charges the allocated
+    capacity for the whole decision interval instead (Eq. 4 with T = step_hours),
+    which is what a provisioned cloud SSD costs whether or not requests run."""
     ci = np.asarray(profile["ci"], np.float64)[:, None]
-    per = request_carbon_g(profile["power"], profile["ttft"], ci, np.asarray(profile["sizes_tb"])[None, :],
-                           platform)
-    return np.asarray(profile["n"], np.float64)[:, None] * per
+    S = np.asarray(profile["sizes_tb"], np.float64)[None, :]
+    n = np.asarray(profile["n"], np.float64)[:, None]
+    if cache_attribution == "ttft":
+        return n * request_carbon_g(profile["power"], profile["ttft"], ci, S, platform)
+    if cache_attribution == "interval":
+        per = request_carbon_g(profile["power"], profile["ttft"], ci, 0.0, platform)
+        return n * per + S * amortised_g(step_hours, platform.ssd_lifetime_years, platform.ssd_kg_per_tb)
+    raise ValueError(f"unknown cache_attribution {cache_attribution!r}")
 
 
 def solve_cache_sizes(cost, ok_ttft, ok_tpot, n_requests, rho=0.9):

@@ -452,7 +452,7 @@ def ilp_profile(seed: int = SEED_BASE + 62, steps: int = 24, sizes_tb=tuple(rang
     hit = 0.7 * (1.0 - np.exp(-S / 6.0))                             # token hit rate vs size
     load = rate[:, None] / 1.8
     ttft = (1.2 + 2.0 * load ** 2) * (1.0 - 0.8 * hit[None, :])      # seconds
-    tpot = 0.12 + 0.1 * load * (1.0 - 0.5 * hit[None, :])
+    tpot = 0.10 + 0.08 * load * (1.0 - 0.5 * hit[None, :])
     power = 1200.0 + 400.0 * load * (1.0 - 0.3 * hit[None, :])        # watts
     spread_ttft = 0.35 * ttft
     z_ttft = (slo_ttft_s - ttft) / spread_ttft
