@@ -2,9 +2,9 @@
 """Benchmark of the prefix-cached prefill path on one MI355X.
 
 One step = the whole hot path over one batch already resident in HBM:
-KV append of the new tokens (gc_kv_append), work-list planning
-(gc_prefix_prefill_plan) and attention (gc_prefix_prefill_run). With
---kv fp8 the pools hold 8-bit E4M3 codes (gc_kv_append_fp8 and
+KV append of the new tokens and work-list planning in one launch
+(gc_prefix_prefill_prepare), then the attention (gc_prefix_prefill_run). With
+--kv fp8 the pools hold 8-bit E4M3 codes (gc_prefix_prefill_prepare_fp8 and
 gc_prefix_prefill_run_fp8; products still bf16 x bf16 -> fp32). The default
 workload is the Llama-3-8B attention shape (32 query / 8 KV heads, head_dim
 128, 8 ragged requests with cached prefixes of 1024-4096 tokens and 64-512
@@ -365,31 +365,30 @@ def main():
     torch.cuda.synchronize()
 
     def step(ev=None):
+        # append and plan in one launch, then the attention
         if ev is not None:
             ev[0].record()
         if fp8:
-            gc.kv_append_fp8(k_new, v_new, k_pool, v_pool, batch, K_SCALE_FP8, V_SCALE_FP8)
+            gc.prepare(k_new, v_new, k_pool, v_pool, batch, Hq, ws, args.kv_split_tiles,
+                       k_scale=K_SCALE_FP8, v_scale=V_SCALE_FP8)
         else:
-            gc.kv_append(k_new, v_new, k_pool, v_pool, batch)
+            gc.prepare(k_new, v_new, k_pool, v_pool, batch, Hq, ws, args.kv_split_tiles)
         if ev is not None:
             ev[1].record()
-        gc.plan(Hq, k_pool, v_pool, batch, ws, args.kv_split_tiles)
-        if ev is not None:
-            ev[2].record()
         if fp8:
             gc.run_fp8(q, k_pool, v_pool, batch, w.scale, K_SCALE_FP8, V_SCALE_FP8, ws, out=out,
                        kv_split_tiles=args.kv_split_tiles)
         else:
             gc.run(q, k_pool, v_pool, batch, w.scale, ws, out=out, kv_split_tiles=args.kv_split_tiles)
         if ev is not None:
-            ev[3].record()
+            ev[2].record()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     # timed region: exactly `steps` steps, host clock around the stream
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -397,9 +396,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    app = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    pln = np.array([e[1].elapsed_time(e[2]) for e in evs])
-    att = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    prep = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    att = np.array([e[1].elapsed_time(e[2]) for e in evs])
     t_att = float(np.mean(att)) * 1e-3
 
     achieved = F / t_att / 1e12
@@ -437,7 +435,7 @@ def main():
                                if fp8 else {"type": "bf16"})},
         "new_tokens_per_s": T / (ms_step * 1e-3),
         "attention_tflops": achieved,
-        "kernel_ms": {"append": float(np.mean(app)), "plan": float(np.mean(pln)),
+        "kernel_ms": {"append_and_plan": float(np.mean(prep)),
                       "attention": float(np.mean(att)),
                       "attention_p10": float(np.percentile(att, 10)),
                       "attention_p90": float(np.percentile(att, 90))},

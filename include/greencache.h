@@ -173,6 +173,19 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       hipStream_t stream);
 
 /*
+ * gc_kv_append followed by gc_prefix_prefill_plan, as one launch: the two are
+ * independent (the plan reads only the lengths), so one launch overlaps them
+ * and saves a kernel boundary in a step that appends and attends once per
+ * batch. Arguments, layouts and errors are those of the two calls (the pool
+ * pointers are required); nothing is enqueued if any check fails. Then call
+ * gc_prefix_prefill_run on the same stream.
+ */
+gc_status gc_prefix_prefill_prepare(const gc_geometry* geo, const gc_batch* batch,
+                                    const gc_plan_options* opts, const void* k_new,
+                                    const void* v_new, void* k_pool, void* v_pool,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * 8-bit KV pools. The paper serves its 70B model with 8-bit weights (§6
  * "Experimental setup"); storing the context cache in 8 bits likewise halves
  * the memory a cached token takes, so twice the context fits a given pool, and
@@ -219,6 +232,13 @@ gc_status gc_prefix_prefill_attention_fp8(const gc_geometry* geo, const gc_batch
                                           float k_scale, float v_scale, float scale, void* out,
                                           float* lse, void* workspace, size_t workspace_bytes,
                                           hipStream_t stream);
+
+/* gc_prefix_prefill_prepare over 8-bit pools (gc_kv_append_fp8 + plan, one launch). */
+gc_status gc_prefix_prefill_prepare_fp8(const gc_geometry* geo, const gc_batch* batch,
+                                        const gc_plan_options* opts, const void* k_new,
+                                        const void* v_new, float k_scale, float v_scale,
+                                        void* k_pool8, void* v_pool8, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Calibration, not part of the attention path: read every byte of `buf`

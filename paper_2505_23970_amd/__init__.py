@@ -24,8 +24,8 @@ STATUS_NAMES = {0: "GC_OK", -1: "GC_ERR_NULL_ARG", -2: "GC_ERR_BAD_SHAPE", -3: "
 
 EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefill_plan",
             "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_kv_append_fp8",
-            "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_read_bandwidth_probe",
-            "gc_status_string")
+            "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_prefix_prefill_prepare",
+            "gc_prefix_prefill_prepare_fp8", "gc_read_bandwidth_probe", "gc_status_string")
 READ_PROBE_SINK_WORDS = 2048 * 256
 
 
@@ -94,6 +94,10 @@ def load_library(path: str | None = None):
     for fn in (lib.gc_prefix_prefill_run_fp8, lib.gc_prefix_prefill_attention_fp8):
         fn.restype = i32
         fn.argtypes = [G, Bp, O, vp, vp, vp, f32, f32, f32, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gc_prefix_prefill_prepare.restype = i32
+    lib.gc_prefix_prefill_prepare.argtypes = [G, Bp, O, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gc_prefix_prefill_prepare_fp8.restype = i32
+    lib.gc_prefix_prefill_prepare_fp8.argtypes = [G, Bp, O, vp, vp, f32, f32, vp, vp, vp, ctypes.c_size_t, vp]
     lib.gc_read_bandwidth_probe.restype = i32
     lib.gc_read_bandwidth_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
     lib.gc_status_string.restype = ctypes.c_char_p
@@ -396,3 +400,32 @@ def prefix_prefill_attention_fp8(q, k_pool8, v_pool8, batch: PagedBatch, scale, 
                                              _stream_handle(stream))
     _check("gc_prefix_prefill_attention_fp8", st, lib)
     return out
+
+
+def prepare(k_new, v_new, k_pool, v_pool, batch: PagedBatch, num_q_heads, workspace, kv_split_tiles=None,
+            stream=None, tiling=None, k_scale=None, v_scale=None):
+    """Append the new tokens' K/V and plan the attention in one launch (then call run
+    or run_fp8 with the same options). 8-bit pools (uint8) take k_scale and v_scale."""
+    import torch
+    lib = load_library()
+    fp8 = k_pool.dtype == torch.uint8
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _require(t, torch.bfloat16, name, batch.device)
+    for name, t in (("k_pool", k_pool), ("v_pool", v_pool)):
+        _require(t, torch.uint8 if fp8 else torch.bfloat16, name, batch.device)
+    _require(workspace, torch.uint8, "workspace", batch.device)
+    geo = _geo_from_pools(k_pool, v_pool, num_q_heads, batch)
+    T, Hkv, D = k_new.shape
+    if (T, Hkv, D) != (batch.total_new, geo.num_kv_heads, geo.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [T][Hkv][D] matching the batch and pools")
+    head = (ctypes.byref(geo), ctypes.byref(batch.desc()), _opts(kv_split_tiles, tiling), k_new.data_ptr(),
+            v_new.data_ptr())
+    tail = (k_pool.data_ptr(), v_pool.data_ptr(), workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    if fp8:
+        if k_scale is None or v_scale is None:
+            raise ValueError("8-bit pools need k_scale and v_scale")
+        st = lib.gc_prefix_prefill_prepare_fp8(*head, float(k_scale), float(v_scale), *tail)
+        _check("gc_prefix_prefill_prepare_fp8", st, lib)
+    else:
+        st = lib.gc_prefix_prefill_prepare(*head, *tail)
+        _check("gc_prefix_prefill_prepare", st, lib)

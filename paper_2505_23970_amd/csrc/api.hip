@@ -203,9 +203,7 @@ gc_status plan_checked(const gc_geometry* geo, const gc_batch* b, const gc_plan_
     return make_plan(geo, b, *sh, o, pl);
 }
 
-gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
-                       void* ws, hipStream_t stream) {
-    (void)geo;
+gc::PlanArgs plan_args(const gc_batch* b, const Shape& sh, const Plan& pl, void* ws) {
     gc::PlanArgs a{};
     a.prefix_lens = b->prefix_lens_dev;
     a.cu_new_lens = b->cu_new_lens_dev;
@@ -223,7 +221,13 @@ gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& s
     a.expect_items = (int32_t)pl.items;
     a.expect_combines = (int32_t)pl.combines;
     a.expect_partials = (int32_t)pl.partials;
-    return gc::launch_plan(a, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+    return a;
+}
+
+gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
+                       void* ws, hipStream_t stream) {
+    (void)geo;
+    return gc::launch_plan(plan_args(b, sh, pl, ws), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
 }
 
 // Pools of bf16 elements (fp8 false, scales 1) or of E4M3 codes with one scale each.
@@ -300,14 +304,9 @@ gc_status check_workspace(const Plan& pl, const void* ws, size_t bytes) {
     return GC_OK;
 }
 
-gc_status append(const gc_geometry* geo, const gc_batch* batch, const void* k_new, const void* v_new,
-                 void* k_pool, void* v_pool, const PoolKind& pk, hipStream_t stream) {
-    Shape sh;
-    gc_status st = check_common(geo, batch, &sh);
-    if (st != GC_OK) return st;
-    if (sh.total_tokens == 0) return GC_OK;
-    if (k_new == nullptr || v_new == nullptr || k_pool == nullptr || v_pool == nullptr)
-        return GC_ERR_NULL_ARG;
+gc::AppendArgs append_args(const gc_geometry* geo, const gc_batch* batch, const Shape& sh,
+                           const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                           const PoolKind& pk) {
     gc::AppendArgs a{};
     a.k_new = static_cast<const uint16_t*>(k_new);
     a.v_new = static_cast<const uint16_t*>(v_new);
@@ -323,7 +322,43 @@ gc_status append(const gc_geometry* geo, const gc_batch* batch, const void* k_ne
     a.max_blocks = geo->max_blocks_per_seq;
     a.k_inv = 1.f / pk.k_scale;  // IEEE division: the same fl32(1 / scale) the definition uses
     a.v_inv = 1.f / pk.v_scale;
+    return a;
+}
+
+gc_status append(const gc_geometry* geo, const gc_batch* batch, const void* k_new, const void* v_new,
+                 void* k_pool, void* v_pool, const PoolKind& pk, hipStream_t stream) {
+    Shape sh;
+    gc_status st = check_common(geo, batch, &sh);
+    if (st != GC_OK) return st;
+    if (sh.total_tokens == 0) return GC_OK;
+    if (k_new == nullptr || v_new == nullptr || k_pool == nullptr || v_pool == nullptr)
+        return GC_ERR_NULL_ARG;
+    const gc::AppendArgs a = append_args(geo, batch, sh, k_new, v_new, k_pool, v_pool, pk);
     return gc::launch_append(a, geo->head_dim, pk.fp8, stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+}
+
+// Append and plan in one launch (the plan reads only the lengths, so the two are
+// independent).
+gc_status prepare(const gc_geometry* geo, const gc_batch* batch, const gc_plan_options* opts,
+                  const void* k_new, const void* v_new, void* k_pool, void* v_pool, void* workspace,
+                  size_t workspace_bytes, hipStream_t stream, const PoolKind& pk) {
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    if (k_new == nullptr || v_new == nullptr || k_pool == nullptr || v_pool == nullptr)
+        return GC_ERR_NULL_ARG;
+    if (pk.fp8) {
+        st = check_pool_scales(pk.k_scale, pk.v_scale);
+        if (st != GC_OK) return st;
+    }
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != GC_OK) return st;
+    const gc::AppendArgs aa = append_args(geo, batch, sh, k_new, v_new, k_pool, v_pool, pk);
+    return gc::launch_prepare(aa, plan_args(batch, sh, pl, workspace), geo->head_dim, pk.fp8, stream) ==
+                   hipSuccess
+               ? GC_OK
+               : GC_ERR_HIP;
 }
 
 gc_status run(const gc_geometry* geo, const gc_batch* batch, const gc_plan_options* opts,
@@ -431,6 +466,24 @@ gc_status gc_prefix_prefill_attention_fp8(const gc_geometry* geo, const gc_batch
                                           hipStream_t stream) {
     return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
                stream, true, PoolKind{true, k_scale, v_scale});
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_prepare(const gc_geometry* geo, const gc_batch* batch,
+                                    const gc_plan_options* opts, const void* k_new, const void* v_new,
+                                    void* k_pool, void* v_pool, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+    return prepare(geo, batch, opts, k_new, v_new, k_pool, v_pool, workspace, workspace_bytes, stream,
+                   PoolKind{});
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_prepare_fp8(const gc_geometry* geo, const gc_batch* batch,
+                                        const gc_plan_options* opts, const void* k_new, const void* v_new,
+                                        float k_scale, float v_scale, void* k_pool8, void* v_pool8,
+                                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return prepare(geo, batch, opts, k_new, v_new, k_pool8, v_pool8, workspace, workspace_bytes, stream,
+                   PoolKind{true, k_scale, v_scale});
 }
 
 __attribute__((visibility("default")))

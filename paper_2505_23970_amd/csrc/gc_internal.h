@@ -174,6 +174,8 @@ struct CombineArgs {
 
 hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
+// append (AppendArgs) and plan (PlanArgs) in one launch
+hipError_t launch_prepare(const AppendArgs& aa, const PlanArgs& pa, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
                             hipStream_t s);
 hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, bool fp8,

@@ -211,3 +211,23 @@ def test_fp8_entry_points_check_scales_on_the_host(lib):
     e = HostBatch([], [], fake_dev=False)
     assert lib.gc_kv_append_fp8(ctypes.byref(g), ctypes.byref(e.desc), None, None, 0.5, 0.5, None,
                                 None, None) == 0
+
+
+def test_prepare_entry_points_check_on_the_host(lib):
+    b = HostBatch([4], [3])
+    g = geo()
+    p = 0x2000
+
+    def prep(kn=p, vn=p, kp=p, ws_bytes=1 << 40):
+        return lib.gc_prefix_prefill_prepare(ctypes.byref(g), ctypes.byref(b.desc), ctypes.byref(NEVER_SPLIT),
+                                             kn, vn, kp, p, 0x3000, ws_bytes, None)
+
+    assert prep(kn=None) == -1
+    assert prep(vn=None) == -1
+    assert prep(kp=None) == -1
+    assert prep(ws_bytes=1) == -5
+    assert lib.gc_prefix_prefill_prepare_fp8(ctypes.byref(g), ctypes.byref(b.desc), ctypes.byref(NEVER_SPLIT),
+                                             p, p, 0.0, 1.0, p, p, 0x3000, 1 << 40, None) == -2
+    e = HostBatch([], [], fake_dev=False)
+    assert lib.gc_prefix_prefill_prepare(ctypes.byref(g), ctypes.byref(e.desc), None, None, None, None, None,
+                                         None, 0, None) == 0

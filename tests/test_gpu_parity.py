@@ -429,3 +429,41 @@ def test_fp8_decode_workload_sampled():
     w = W.decode_variant()
     info = fp8_check(w, 2.0 ** -6, 0.0213, rows=H.sample_rows(w, seed=51))
     say(f"8-bit decode, 32 requests: {info}")
+
+
+# ----------------------------------------------------------------- append and plan in one launch
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+@pytest.mark.parametrize("split", [None, 2])
+def test_prepare_equals_append_then_plan(kv, split):
+    """gc_prefix_prefill_prepare (append and plan in one launch) followed by run gives
+    the separate calls' pools and outputs bit for bit."""
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build(seed=112, name=f"prepare_{kv}", **SUITE_SHAPE)
+    say(f"case {w.name}: split {split}")
+    if kv == "fp8":
+        a, b = H.DeviceRunFp8(w, 0.0113, 0.0271), H.DeviceRunFp8(w, 0.0113, 0.0271)
+        extra = dict(k_scale=a.ks, v_scale=a.vs)
+    else:
+        a, b = H.DeviceRun(w), H.DeviceRun(w)
+        extra = {}
+    a.append()
+    out_a, lse_a = a.attention(kv_split_tiles=split)
+    T, Hq, D = w.q.shape
+    ws = gc.alloc_workspace(Hq, b.k_pool, b.v_pool, b.batch, split)
+    gc.prepare(b.k_new, b.v_new, b.k_pool, b.v_pool, b.batch, Hq, ws, kv_split_tiles=split, **extra)
+    lse_b = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    out_b = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    if kv == "fp8":
+        gc.run_fp8(b.q, b.k_pool, b.v_pool, b.batch, w.scale, b.ks, b.vs, ws, out=out_b, lse=lse_b,
+                   kv_split_tiles=split)
+    else:
+        gc.run(b.q, b.k_pool, b.v_pool, b.batch, w.scale, ws, out=out_b, lse=lse_b, kv_split_tiles=split)
+    torch.cuda.synchronize()
+    # Unused pool slots hold NaN sentinels, so every comparison is on the bits.
+    bits = {1: torch.uint8, 2: torch.int16, 4: torch.int32}
+    same = lambda x, y: torch.equal(x.view(bits[x.element_size()]), y.view(bits[y.element_size()]))
+    assert same(a.k_pool, b.k_pool) and same(a.v_pool, b.v_pool)
+    assert same(out_a, out_b)
+    assert same(lse_a, lse_b)
