@@ -186,6 +186,34 @@ gc_status gc_prefix_prefill_prepare(const gc_geometry* geo, const gc_batch* batc
                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * gc_kv_append and gc_prefix_prefill_run fused (§2.2: the new tokens are
+ * processed together with the reused prefix and their KV is saved for later
+ * requests). With prefill tiles one launch does both: the attention reads every
+ * key at or past P_r straight from k_new / v_new instead of the pool (so it does
+ * not wait for the append, and the append's workgroups run in the same launch
+ * after the attention's). With small tiles (decode-like batches), whose kernel
+ * reads every key from the pool, the append is enqueued first as its own launch.
+ *   q, k_new, v_new: device bf16 [T][Hq][D], [T][Hkv][D], [T][Hkv][D]
+ *   k_pool, v_pool : device bf16 pools, updated in place exactly as by
+ *                    gc_kv_append
+ *   other arguments: as gc_prefix_prefill_run (a plan made by
+ *                    gc_prefix_prefill_plan for this batch and these options
+ *                    must be in the workspace)
+ * Pools, out and lse are bit for bit those of gc_kv_append followed by
+ * gc_prefix_prefill_run. A pool page that receives new tokens must not be read
+ * as part of another request's prefix in the same batch (with the separate calls
+ * such a read would see the appended tokens, here it may not). Errors as the two
+ * calls, plus GC_ERR_UNSUPPORTED when a request's new rows span 2 GiB or more
+ * (n_r * Hkv * D * 2 bytes > 2^31 - 1); nothing is enqueued if any check fails.
+ */
+gc_status gc_prefix_prefill_run_with_append(const gc_geometry* geo, const gc_batch* batch,
+                                            const gc_plan_options* opts, const void* q,
+                                            const void* k_new, const void* v_new,
+                                            void* k_pool, void* v_pool, float scale,
+                                            void* out, float* lse, void* workspace,
+                                            size_t workspace_bytes, hipStream_t stream);
+
+/*
  * 8-bit KV pools. The paper serves its 70B model with 8-bit weights (§6
  * "Experimental setup"); storing the context cache in 8 bits likewise halves
  * the memory a cached token takes, so twice the context fits a given pool, and

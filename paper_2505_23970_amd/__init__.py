@@ -25,7 +25,8 @@ STATUS_NAMES = {0: "GC_OK", -1: "GC_ERR_NULL_ARG", -2: "GC_ERR_BAD_SHAPE", -3: "
 EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefill_plan",
             "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_kv_append_fp8",
             "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_prefix_prefill_prepare",
-            "gc_prefix_prefill_prepare_fp8", "gc_read_bandwidth_probe", "gc_status_string")
+            "gc_prefix_prefill_prepare_fp8", "gc_prefix_prefill_run_with_append", "gc_read_bandwidth_probe",
+            "gc_status_string")
 READ_PROBE_SINK_WORDS = 2048 * 256
 
 
@@ -98,6 +99,9 @@ def load_library(path: str | None = None):
     lib.gc_prefix_prefill_prepare.argtypes = [G, Bp, O, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.gc_prefix_prefill_prepare_fp8.restype = i32
     lib.gc_prefix_prefill_prepare_fp8.argtypes = [G, Bp, O, vp, vp, f32, f32, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gc_prefix_prefill_run_with_append.restype = i32
+    lib.gc_prefix_prefill_run_with_append.argtypes = [G, Bp, O, vp, vp, vp, vp, vp, f32, vp, vp, vp,
+                                                      ctypes.c_size_t, vp]
     lib.gc_read_bandwidth_probe.restype = i32
     lib.gc_read_bandwidth_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
     lib.gc_status_string.restype = ctypes.c_char_p
@@ -307,6 +311,26 @@ def run(q, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=No
                                    lse.data_ptr() if lse is not None else None,
                                    workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
     _check("gc_prefix_prefill_run", st, lib)
+    return out
+
+
+def run_with_append(q, k_new, v_new, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=None,
+                    kv_split_tiles=None, stream=None, tiling=None):
+    """Append the new tokens' K/V (bf16 [T][Hkv][D]) into the pools and run the attention,
+    in one launch with prefill tiles, from a plan already in `workspace`."""
+    import torch
+    lib = load_library()
+    geo, out = _attn_args(q, k_pool, v_pool, batch, out, lse, workspace)
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _require(t, torch.bfloat16, name, batch.device)
+    if tuple(k_new.shape) != (batch.total_new, geo.num_kv_heads, geo.head_dim) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [T][Hkv][D] matching the batch and pools")
+    st = lib.gc_prefix_prefill_run_with_append(
+        ctypes.byref(geo), ctypes.byref(batch.desc()), _opts(kv_split_tiles, tiling), q.data_ptr(),
+        k_new.data_ptr(), v_new.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), float(scale), out.data_ptr(),
+        lse.data_ptr() if lse is not None else None, workspace.data_ptr(), workspace.numel(),
+        _stream_handle(stream))
+    _check("gc_prefix_prefill_run_with_append", st, lib)
     return out
 
 

@@ -238,7 +238,8 @@ struct PoolKind {
 
 gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
                       const void* q, const void* k_pool, const void* v_pool, float scale,
-                      void* out, float* lse, void* ws, hipStream_t stream, const PoolKind& pk = PoolKind{}) {
+                      void* out, float* lse, void* ws, hipStream_t stream, const PoolKind& pk = PoolKind{},
+                      const gc::AppendArgs* fused = nullptr) {
     gc::AttnArgs a{};
     a.q = static_cast<const uint16_t*>(q);
     a.k_pool = static_cast<const uint16_t*>(k_pool);
@@ -259,8 +260,17 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
     a.max_blocks = geo->max_blocks_per_seq;
     a.scale_log2 = (float)((double)scale * (double)pk.k_scale * 1.4426950408889634074);
     a.v_scale = pk.v_scale;
-    const hipError_t e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, pk.fp8, stream)
-                                  : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, pk.fp8, stream);
+    hipError_t e;
+    if (fused != nullptr) {  // prefill tiles over bf16 pools only
+        a.k_new = fused->k_new;
+        a.v_new = fused->v_new;
+        a.k_dst = static_cast<uint16_t*>(fused->k_pool);
+        a.v_dst = static_cast<uint16_t*>(fused->v_pool);
+        e = gc::launch_attention_append(a, geo->head_dim, pl.items, sh.wide, stream);
+    } else {
+        e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, pk.fp8, stream)
+                     : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, pk.fp8, stream);
+    }
     if (e != hipSuccess) return GC_ERR_HIP;
     if (pl.combines > 0) {
         gc::CombineArgs c{};
@@ -384,6 +394,36 @@ gc_status run(const gc_geometry* geo, const gc_batch* batch, const gc_plan_optio
     return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream, pk);
 }
 
+// Append and run from a plan already in the workspace. Prefill tiles: one launch
+// (the work items read the new keys from k_new / v_new and write their own tokens'
+// K/V into the pools). Small tiles read every key from the pool, so there the append
+// is its own launch, before the attention.
+gc_status run_with_append(const gc_geometry* geo, const gc_batch* batch, const gc_plan_options* opts,
+                          const void* q, const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                          float scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    st = check_run_args(q, k_pool, v_pool, scale, out);
+    if (st != GC_OK) return st;
+    if (k_new == nullptr || v_new == nullptr) return GC_ERR_NULL_ARG;
+    st = check_workspace(pl, workspace, workspace_bytes);
+    if (st != GC_OK) return st;
+    // the attention addresses a request's new rows with 32-bit offsets
+    const int64_t row_bytes = (int64_t)geo->num_kv_heads * geo->head_dim * 2;
+    for (int r = 0; r < batch->batch; ++r)
+        if ((int64_t)batch->new_lens_host[r] * row_bytes > INT32_MAX) return GC_ERR_UNSUPPORTED;
+    const gc::AppendArgs aa = append_args(geo, batch, sh, k_new, v_new, k_pool, v_pool, PoolKind{});
+    if (sh.small) {
+        if (gc::launch_append(aa, geo->head_dim, false, stream) != hipSuccess) return GC_ERR_HIP;
+        return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream);
+    }
+    return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream, PoolKind{},
+                       &aa);
+}
+
 }  // namespace
 
 extern "C" {
@@ -445,6 +485,16 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       size_t workspace_bytes, hipStream_t stream) {
     return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
                stream, true, PoolKind{});
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_run_with_append(const gc_geometry* geo, const gc_batch* batch,
+                                            const gc_plan_options* opts, const void* q, const void* k_new,
+                                            const void* v_new, void* k_pool, void* v_pool, float scale,
+                                            void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                            hipStream_t stream) {
+    return run_with_append(geo, batch, opts, q, k_new, v_new, k_pool, v_pool, scale, out, lse, workspace,
+                           workspace_bytes, stream);
 }
 
 __attribute__((visibility("default")))

@@ -44,6 +44,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kLn2 = 0.69314718055994530942f;
+// Buffer resource word 3 for raw (untyped) loads: 32-bit data format.
+constexpr int kBufferFlags = 0x00020000;
 
 // 16-byte chunk position inside an LDS row (conflict-free 16-lane reads).
 template <int D>
@@ -95,8 +97,12 @@ __device__ __forceinline__ void widen_e4m3x16(const u32x4 c, u32x4& lo, u32x4& h
     hi = u32x4{w[4], w[5], w[6], w[7]};
 }
 
-template <int D, int WAVES, bool FP8>
-__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const AttnArgs a) {
+// One work item (a workgroup of WAVES wavefronts). FUSE: the KV append runs in the
+// same launch, so the keys at or past the prefix length are taken from the new
+// tokens' arrays, not from the pool (bf16 pools only).
+template <int D, int WAVES, bool FP8, bool FUSE>
+__device__ __forceinline__ void attention_body(const AttnArgs& a) {
+    static_assert(!(FP8 && FUSE), "the fused append runs over bf16 pools");
     constexpr int kBlockRows = WAVES * kRowsPerWave;  // query rows of a work item
     constexpr int DK = D / 16;                      // k-steps of QK^T
     constexpr int DB = D / 32;                      // 32-row blocks of O^T
@@ -156,13 +162,25 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
     static_assert(WAVES % kKbPerPage == 0, "piece layout");
     auto page_of = [&](int e) -> int { return (WAVES / kKbPerPage) * e + (wave & (WAVES - 1)) / kKbPerPage; };
     const int k_row = sub * (1024 / (2 * D)) + lane / (D / 8);         // key slot in the page
-    const uint32_t k_src = k_row * (2 * D) + swz_k<D>(lane % (D / 8), k_row) * 16;
+    const uint32_t k_chunk = swz_k<D>(lane % (D / 8), k_row) * 16;     // source chunk of the row
+    const uint32_t k_src = k_row * (2 * D) + k_chunk;
     const int v_d = sub * 32 + (lane >> 1);                            // value row (d) in the page
     const int v_half = (lane & 1) ^ ((v_d >> 3) & 1);                  // logical half held by the lane
     const uint32_t v_src = v_d * 32 + v_half * 16;
     const int32_t* table = a.block_tables + (int64_t)r * a.max_blocks;
     const int64_t head_off = (int64_t)kvh * kPageBytes;
     const int64_t block_stride = (int64_t)a.num_kv_heads * kPageBytes;
+    // fused append: this KV head's rows of the request's new tokens (new key P + i at
+    // row i) and the byte stride between consecutive tokens
+    const int64_t new_stride = (int64_t)a.num_kv_heads * D * 2;
+    auto new_rows = [&](const uint16_t* base) {
+        return reinterpret_cast<const unsigned char*>(base) + ((int64_t)cu * a.num_kv_heads + kvh) * D * 2;
+    };
+    const unsigned char* k_new_h = FUSE ? new_rows(a.k_new) : nullptr;
+    // the values as a buffer of exactly these rows' bytes (the host keeps them < 2 GiB)
+    const __amdgpu_buffer_rsrc_t v_new_r = __builtin_amdgcn_make_buffer_rsrc(
+        FUSE ? (void*)new_rows(a.v_new) : nullptr, (short)0,
+        FUSE ? (int)((int64_t)max(n - 1, 0) * new_stride + 2 * D) : 0, kBufferFlags);
 
     // raw table entries of tile kt (indices clamped into the row; checked at use)
     // (a vector load: lane p of every 4 holds entry p; it completes with the tile loads,
@@ -180,8 +198,16 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
                 const int64_t base = (int64_t)blk * block_stride + head_off;
                 const unsigned char* kg = reinterpret_cast<const unsigned char*>(a.k_pool) + base;
                 const unsigned char* vg = reinterpret_cast<const unsigned char*>(a.v_pool) + base;
-                dma16(kg + k_src, kdst + pg * kPageBytes + sub * 1024);
-                dma16(vg + v_src, vdst + pg * kPageBytes + sub * 1024);
+                const unsigned char* ks = kg + k_src;
+                if constexpr (FUSE) {
+                    if (lp * kPage + kPage > P) {           // the page holds new keys
+                        const int pos = lp * kPage + k_row;  // this lane's key
+                        if (pos >= P && pos < L) ks = k_new_h + (int64_t)(pos - P) * new_stride + k_chunk;
+                    }
+                }
+                dma16(ks, kdst + pg * kPageBytes + sub * 1024);
+                // (fused: a page of new keys only takes its values from registers)
+                if (!FUSE || lp * kPage < P) dma16(vg + v_src, vdst + pg * kPageBytes + sub * 1024);
             }
         }
     };
@@ -201,6 +227,70 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
         }
     };
 
+    // Fused append, values of new keys. Their rows are token-major, the LDS tile is
+    // transposed, so they go through registers: the lanes of a wavefront cover exactly
+    // the 1 KiB pieces its own copies fill (32 value rows x 16 keys of one page), one
+    // (8 keys, 2 value rows) task per lane and pass: eight 4-byte loads issued with the
+    // tile's copies and held during the previous tile's products, then two 16-byte
+    // LDS writes (element writes in the group that holds the first new key, whose
+    // prefix keys come from the pool). The loads go through a buffer resource over the
+    // request's rows, so a key before the prefix end (negative offset) or at or past
+    // the sequence end reads as 0 without a test; a tile's offsets stay within
+    // (-64, n) rows of the first new key.
+    constexpr int kNewTasks = 32 * NI;  // per wavefront and tile
+    constexpr int NV = FUSE ? (kNewTasks + 63) / 64 : 1;
+    uint32_t nv[NV][8];
+    auto has_new = [&](int kt) { return kt * kBlockN + kBlockN > P; };
+    auto task_of = [&](int j, int& pg, int& d0, int& half) {
+        const int t = lane + 64 * j;
+        pg = page_of(t >> 5);
+        d0 = 32 * sub + 2 * (t & 15);
+        half = (t >> 4) & 1;
+        return t < kNewTasks;
+    };
+    auto load_newv = [&](int kt) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            int pg, d0, half;
+            const bool ok = task_of(j, pg, d0, half);
+            const int key0 = kt * kBlockN + pg * kPage + half * 8;
+            const int stride = (int)new_stride;
+            const int off = ok ? (key0 - P) * stride + d0 * 2 : INT32_MIN / 2;  // lanes without a task read 0
+#pragma unroll
+            for (int x = 0; x < 8; ++x) nv[j][x] = __builtin_amdgcn_raw_buffer_load_b32(v_new_r, off + x * stride, 0, 0);
+        }
+    };
+    auto store_newv = [&](unsigned char* vdst, int kt) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            int pg, d0, half;
+            if (!task_of(j, pg, d0, half)) continue;
+            const int key0 = kt * kBlockN + pg * kPage + half * 8;
+            if (key0 + 8 <= P) continue;  // eight prefix keys: the page copy holds them
+            u32x4 r0, r1;                 // rows d0 and d0 + 1 of the eight keys
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                r0[i] = (nv[j][2 * i] & 0xFFFFu) | (nv[j][2 * i + 1] << 16);
+                r1[i] = (nv[j][2 * i] >> 16) | (nv[j][2 * i + 1] & 0xFFFF0000u);
+            }
+            // d0 is even, so rows d0 and d0 + 1 share the half swap
+            unsigned char* row = vdst + pg * kPageBytes + d0 * 32 + ((half ^ ((d0 >> 3) & 1)) * 16);
+            if (key0 >= P) {
+                *reinterpret_cast<u32x4*>(row) = r0;
+                *reinterpret_cast<u32x4*>(row + 32) = r1;
+            } else {
+                uint16_t* w0 = reinterpret_cast<uint16_t*>(row);
+                uint16_t* w1 = reinterpret_cast<uint16_t*>(row + 32);
+#pragma unroll
+                for (int x = 0; x < 8; ++x)
+                    if (key0 + x >= P) {
+                        w0[x] = (uint16_t)(nv[j][x] & 0xFFFFu);
+                        w1[x] = (uint16_t)(nv[j][x] >> 16);
+                    }
+            }
+        }
+    };
+
     f32x16 o[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[db] = f32x16{};
@@ -213,7 +303,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
 
     // LDS fragment reads kept in flight ahead of their MFMA (fewer when 8-bit codes
     // for the next tile occupy registers during the products)
-    constexpr int kAhead = (FP8 && WAVES == 4 && D == 128) ? 4 : 6;
+    constexpr int kAhead = ((FP8 || FUSE) && WAVES == 4 && D == 128) ? 4 : 6;
     auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt) {
         // S^T = K_tile . Q^T: MFMA i uses K fragment (k = i/2, block b = i%2). Every
         // group below is fenced so the fragment reads stay kAhead MFMAs ahead.
@@ -382,27 +472,92 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
         }
     };
 
+    // Fused append, pool writes: the keys and values of this work item's own tokens
+    // (positions P + q0 .. P + q0 + ntok - 1) go from the LDS tile that holds them to
+    // their pool slots, bit for bit. Each (token, KV head) has exactly one writer: the
+    // query tile that owns the token, in the key chunk that covers its position. bl
+    // holds the raw block-table entries of tile kt's four pages (wave-uniform); pages
+    // past the table or with a bad id are skipped, as the plain append does.
+    auto write_own = [&](const unsigned char* kb, const unsigned char* vb, int kt, const int (&bl)[4]) {
+        const int lo = max(P + it.q0, kt * kBlockN), hi = min(P + it.q0 + ntok, kt * kBlockN + kBlockN);
+        if (lo >= hi) return;
+        constexpr int CPR = D / 8;  // 16-byte chunks per key row
+        constexpr int THREADS = WAVES * 64;
+        const int64_t page_elems = (int64_t)kPage * D;  // elements of one (block, KV head) page
+        int blk4[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+            blk4[p] = (kt * 4 + p < a.max_blocks && bl[p] >= 0 && bl[p] < a.num_blocks) ? bl[p] : -1;
+        auto page_block = [&](int key) {
+            const int p = key / kPage - kt * 4;
+            return p == 0 ? blk4[0] : p == 1 ? blk4[1] : p == 2 ? blk4[2] : blk4[3];
+        };
+        for (int u = tid; u < (hi - lo) * CPR; u += THREADS) {
+            const int key = lo + u / CPR, c = u % CPR;
+            const int b = page_block(key);
+            if (b < 0) continue;
+            const int rt = key - kt * kBlockN;  // row in the tile
+            const u32x4 v = *reinterpret_cast<const u32x4*>(kb + rt * (2 * D) + swz_k<D>(c, rt) * 16);
+            *reinterpret_cast<u32x4*>(a.k_dst + ((int64_t)b * a.num_kv_heads + kvh) * page_elems +
+                                      (key % kPage) * D + c * 8) = v;
+        }
+        // values: (page, row d, half h) units of 8 slots
+        const int p0 = lo / kPage, np = (hi - 1) / kPage - p0 + 1;
+        for (int u = tid; u < np * 2 * D; u += THREADS) {
+            const int lp = p0 + u / (2 * D), d = (u % (2 * D)) >> 1, h = u & 1;
+            const int k0 = lp * kPage + 8 * h;
+            const int a0 = max(k0, lo), a1 = min(k0 + 8, hi);
+            if (a0 >= a1) continue;
+            const int b = page_block(k0);
+            if (b < 0) continue;
+            const unsigned char* src = vb + (lp - kt * 4) * kPageBytes + d * 32 + ((h ^ ((d >> 3) & 1)) * 16);
+            uint16_t* dst = a.v_dst + ((int64_t)b * a.num_kv_heads + kvh) * page_elems + d * kPage + 8 * h;
+            if (a1 - a0 == 8) {
+                *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+            } else {
+                const uint16_t* s16 = reinterpret_cast<const uint16_t*>(src);
+                for (int x = 0; x < 8; ++x)
+                    if (k0 + x >= a0 && k0 + x < a1) dst[x] = s16[x];
+            }
+        }
+    };
+
     // One pipeline step: start the next tile's loads into the other buffers, compute
     // this tile, make the next tile visible.
-    int ids;
+    int ids;        // block-table entries of the next tile to copy (entry p in lanes with lane % 4 == p)
+    int bl_cur[4];  // (fused append) the entries of the tile being computed, wave-uniform
+    auto take_ids = [&](int (&bl)[4]) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) bl[p] = __builtin_amdgcn_readlane(ids, p);
+    };
     int kt = it.kt_begin;
     auto step = [&](unsigned char* kc, unsigned char* vc, unsigned char* kn, unsigned char* vn) {
         const bool more = kt + 1 < it.kt_end;
+        int bl_next[4];
+        if constexpr (FUSE) take_ids(bl_next);
         if (more) {
             if constexpr (FP8) load8(kt + 1, ids);
             else issue_tile(kn, vn, kt + 1, ids);
+            if constexpr (FUSE)
+                if (has_new(kt + 1)) load_newv(kt + 1);
             if (kt + 2 < it.kt_end) fetch_ids(kt + 2, ids);
         }
+        if constexpr (FUSE) write_own(kc, vc, kt, bl_cur);
         compute_tile(kc, vc, kt);
         if (more) {
             if constexpr (FP8) {
                 store8(kn, vn, kt + 1);
             } else {
                 wait_vmem<0>();
+                if constexpr (FUSE)
+                    if (has_new(kt + 1)) store_newv(vn, kt + 1);
                 zero_tail(vn, kt + 1);
             }
         }
         __syncthreads();
+        if constexpr (FUSE)
+#pragma unroll
+            for (int p = 0; p < 4; ++p) bl_cur[p] = bl_next[p];
     };
 
     fetch_ids(kt, ids);
@@ -412,8 +567,13 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
         store8(k_lds0, v_lds0, kt);
     } else {
         issue_tile(k_lds0, v_lds0, kt, ids);
+        if constexpr (FUSE) take_ids(bl_cur);
+        if constexpr (FUSE)
+            if (has_new(kt)) load_newv(kt);
         if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
         wait_vmem<0>();
+        if constexpr (FUSE)
+            if (has_new(kt)) store_newv(v_lds0, kt);
         zero_tail(v_lds0, kt);
     }
     __syncthreads();
@@ -455,6 +615,19 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
             }
         if (hh == 0) a.part_lse[prow_g] = lse_v;
     }
+}
+
+template <int D, int WAVES, bool FP8>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const AttnArgs a) {
+    attention_body<D, WAVES, FP8, false>(a);
+}
+
+// Attention with the KV append fused in: the work items read new keys from the new
+// tokens' arrays (so they do not wait for any append) and write their own tokens'
+// keys and values into the pools from LDS.
+template <int D, int WAVES>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_append_kernel(const AttnArgs a) {
+    attention_body<D, WAVES, false, true>(a);
 }
 
 // Merge the key chunks of one split query tile: with m = max_s lse_s,
@@ -550,6 +723,23 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, 
         launch_prefill<true>(a, head_dim, grid, wide, s);
     else
         launch_prefill<false>(a, head_dim, grid, wide, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_append(const AttnArgs& a, int head_dim, int64_t num_items, bool wide,
+                                   hipStream_t s) {
+    const dim3 grid((unsigned)(num_items * a.num_kv_heads));
+    if (wide) {
+        if (head_dim == 128)
+            attention_append_kernel<128, kWideWaves><<<grid, kWideWaves * 64, 0, s>>>(a);
+        else
+            attention_append_kernel<64, kWideWaves><<<grid, kWideWaves * 64, 0, s>>>(a);
+    } else {
+        if (head_dim == 128)
+            attention_append_kernel<128, kWaves><<<grid, kWaves * 64, 0, s>>>(a);
+        else
+            attention_append_kernel<64, kWaves><<<grid, kWaves * 64, 0, s>>>(a);
+    }
     return hipGetLastError();
 }
 

@@ -158,6 +158,14 @@ struct AttnArgs {
     int32_t num_blocks, max_blocks;
     float scale_log2;    // softmax scale * log2(e) (times the key scale for 8-bit pools)
     float v_scale;       // value scale of 8-bit pools, 1 for bf16 pools
+    // Append fused into the launch: keys at or past a request's prefix length are read
+    // from the new tokens' arrays ([T][Hkv][D]) instead of the pool, and each work item
+    // writes its own tokens' keys and values into the pools (k_dst / v_dst, the same
+    // memory as k_pool / v_pool). Null otherwise.
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    uint16_t* k_dst;
+    uint16_t* v_dst;
 };
 
 struct CombineArgs {
@@ -178,6 +186,10 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_prepare(const AppendArgs& aa, const PlanArgs& pa, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
                             hipStream_t s);
+// attention with the KV append fused in (AttnArgs with k_new, v_new, k_dst, v_dst
+// set); prefill tiles over bf16 pools
+hipError_t launch_attention_append(const AttnArgs& a, int head_dim, int64_t num_items, bool wide,
+                                   hipStream_t s);
 hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, bool fp8,
                                   hipStream_t s);
 hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);

@@ -231,3 +231,26 @@ def test_prepare_entry_points_check_on_the_host(lib):
     e = HostBatch([], [], fake_dev=False)
     assert lib.gc_prefix_prefill_prepare(ctypes.byref(g), ctypes.byref(e.desc), None, None, None, None, None,
                                          None, 0, None) == 0
+
+
+def test_run_with_append_checks_on_the_host(lib):
+    b = HostBatch([4], [3])
+    g = geo()
+    p = 0x2000
+
+    def call(q=p, kn=p, vn=p, kp=p, scale=0.125, out=p, ws_bytes=1 << 40, batch=b):
+        return lib.gc_prefix_prefill_run_with_append(ctypes.byref(g), ctypes.byref(batch.desc),
+                                                     ctypes.byref(NEVER_SPLIT), q, kn, vn, kp, p, scale, out,
+                                                     None, 0x3000, ws_bytes, None)
+
+    assert call(kn=None) == -1
+    assert call(vn=None) == -1
+    assert call(q=None) == -1
+    assert call(kp=None) == -1
+    assert call(out=None) == -1
+    assert call(scale=0.0) == -2
+    assert call(scale=float("nan")) == -2
+    assert call(ws_bytes=1) == -5
+    # nothing to do for a batch without new tokens, whatever the pointers
+    e = HostBatch([], [], fake_dev=False)
+    assert call(q=None, kn=None, vn=None, kp=None, out=None, ws_bytes=0, batch=e) == 0

@@ -467,3 +467,87 @@ def test_prepare_equals_append_then_plan(kv, split):
     assert same(a.k_pool, b.k_pool) and same(a.v_pool, b.v_pool)
     assert same(out_a, out_b)
     assert same(lse_a, lse_b)
+
+
+# ----------------------------------------------------------------- append fused into the attention launch
+
+def same_bits(x, y):
+    """Bitwise equality of two device tensors (unused pool slots hold NaN sentinels)."""
+    import torch
+    bits = {1: torch.uint8, 2: torch.int16, 4: torch.int32}
+    return torch.equal(x.view(bits[x.element_size()]), y.view(bits[y.element_size()]))
+
+
+def fused_run(run: H.DeviceRun, kv_split_tiles=None, tiling=None):
+    """gc_prefix_prefill_plan, then gc_prefix_prefill_run_with_append on `run`'s
+    initial pools; returns out and lse."""
+    import torch
+    import paper_2505_23970_amd as gc
+    w = run.w
+    T, Hq, D = w.q.shape
+    ws = gc.alloc_workspace(Hq, run.k_pool, run.v_pool, run.batch, kv_split_tiles, tiling)
+    gc.plan(Hq, run.k_pool, run.v_pool, run.batch, ws, kv_split_tiles=kv_split_tiles, tiling=tiling)
+    lse = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    out = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    gc.run_with_append(run.q, run.k_new, run.v_new, run.k_pool, run.v_pool, run.batch, w.scale, ws, out=out,
+                       lse=lse, kv_split_tiles=kv_split_tiles, tiling=tiling)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+def fused_equals_separate(w, kv_split_tiles=None, tiling=None):
+    """The fused launch gives the separate append + run's pools, output and LSE bit for bit."""
+    import torch
+    say(f"case {w.name}: fused append, B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} "
+        f"D={w.head_dim} T={w.total_new} split={kv_split_tiles} tiling={tiling}")
+    a, b = H.DeviceRun(w), H.DeviceRun(w)
+    a.append()
+    out_a, lse_a = a.attention(kv_split_tiles=kv_split_tiles, tiling=tiling)
+    out_b, lse_b = fused_run(b, kv_split_tiles, tiling)
+    assert same_bits(a.k_pool, b.k_pool) and same_bits(a.v_pool, b.v_pool)
+    if not same_bits(out_a, out_b):
+        bad = torch.nonzero(out_a.view(torch.int16) != out_b.view(torch.int16))[:5].tolist()
+        raise AssertionError(f"outputs differ at {bad}")
+    assert same_bits(lse_a, lse_b)
+
+
+@pytest.mark.parametrize("split", [None, 2])
+@pytest.mark.parametrize("tiling", [None, 1, 3, 2], ids=["auto", "prefill", "wide", "small"])
+def test_fused_append_every_tiling(tiling, split):
+    w = W.build(seed=120, name="fused_suite", values="unit", **SUITE_SHAPE)
+    fused_equals_separate(w, split, tiling)
+
+
+@pytest.mark.parametrize("name,P,n,Hq,Hkv,D", EDGES, ids=[e[0] for e in EDGES])
+def test_fused_append_edge_cases(name, P, n, Hq, Hkv, D):
+    import paper_2505_23970_amd as gc
+    w = W.build(P, n, Hq, Hkv, D, seed=300 + EDGES.index((name, P, n, Hq, Hkv, D)), values="unit",
+                name=name)
+    fused_equals_separate(w)
+    fused_equals_separate(w, kv_split_tiles=1)
+    fused_equals_separate(w, tiling=gc.TILES_WIDE)
+    fused_equals_separate(w, kv_split_tiles=1, tiling=gc.TILES_PREFILL)
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_fused_append_configs(k):
+    fused_equals_separate(W.make_config(k))
+
+
+def test_fused_append_decode_workload():
+    # small tiles: the append is its own launch ahead of the attention
+    fused_equals_separate(W.decode_variant())
+
+
+@pytest.mark.parametrize("split", [None, 3])
+def test_fused_append_against_the_oracle(split):
+    """Pools and every output row of the fused launch against the oracle directly."""
+    w = W.build([130, 0, 64, 1500, 17], [200, 70, 64, 1, 95], 16, 2, 128, seed=125, name="fused_oracle")
+    say(f"case {w.name}: fused append vs oracle, split {split}")
+    kp_ref, vp_ref = H.oracle_pools(w)
+    run = H.DeviceRun(w)
+    out, lse = fused_run(run, kv_split_tiles=split)
+    check_pool(run, kp_ref, vp_ref)
+    ref_out, ref_lse = H.oracle_rows(w, kp_ref, vp_ref)
+    info = H.compare_attention(w, out, lse, ref_out, ref_lse, contract=True)
+    say(f"fused vs oracle: {info}")
