@@ -188,28 +188,43 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     auto fetch_ids = [&](int kt, int& ids) {
         ids = table[min(kt * 4 + (lane & 3), a.max_blocks - 1)];
     };
-    auto issue_tile = [&](unsigned char* kdst, unsigned char* vdst, int kt, const int ids) {
-#pragma unroll
-        for (int e = 0; e < NI; ++e) {
-            const int pg = page_of(e);
-            const int lp = kt * 4 + pg;
-            const int blk = __builtin_amdgcn_readlane(ids, pg);
-            if (lp < a.max_blocks && lp * kPage < L && blk >= 0 && blk < a.num_blocks) {
-                const int64_t base = (int64_t)blk * block_stride + head_off;
-                const unsigned char* kg = reinterpret_cast<const unsigned char*>(a.k_pool) + base;
-                const unsigned char* vg = reinterpret_cast<const unsigned char*>(a.v_pool) + base;
-                const unsigned char* ks = kg + k_src;
-                if constexpr (FUSE) {
-                    if (lp * kPage + kPage > P) {           // the page holds new keys
-                        const int pos = lp * kPage + k_row;  // this lane's key
-                        if (pos >= P && pos < L) ks = k_new_h + (int64_t)(pos - P) * new_stride + k_chunk;
-                    }
-                }
-                dma16(ks, kdst + pg * kPageBytes + sub * 1024);
-                // (fused: a page of new keys only takes its values from registers)
-                if (!FUSE || lp * kPage < P) dma16(vg + v_src, vdst + pg * kPageBytes + sub * 1024);
+    // Copies of piece e of tile kt (one page of K and of V for this wave). Plain
+    // attention: a page past the table, past the sequence or with a block id outside
+    // the pool is copied from block 0 instead (its keys are masked and its values
+    // zeroed after the copy), so the copy needs no branch and can be issued between
+    // the products of the tile before. Fused append: pages that are not copied are
+    // skipped, and a page of new keys takes its values from registers.
+    // (blk: the raw table entry of the page, read from the lanes of `ids` beforehand)
+    auto issue_page = [&](unsigned char* kdst, unsigned char* vdst, int kt, const int blk, int e) {
+        const int pg = page_of(e);
+        const int lp = kt * 4 + pg;
+        const bool ok = lp < a.max_blocks && lp * kPage < L && blk >= 0 && blk < a.num_blocks;
+        const unsigned char* kpool = reinterpret_cast<const unsigned char*>(a.k_pool);
+        const unsigned char* vpool = reinterpret_cast<const unsigned char*>(a.v_pool);
+        if constexpr (!FUSE) {
+            const int64_t base = (int64_t)(ok ? blk : 0) * block_stride + head_off;
+            dma16(kpool + base + k_src, kdst + pg * kPageBytes + sub * 1024);
+            dma16(vpool + base + v_src, vdst + pg * kPageBytes + sub * 1024);
+        } else if (ok) {
+            const int64_t base = (int64_t)blk * block_stride + head_off;
+            const unsigned char* ks = kpool + base + k_src;
+            if (lp * kPage + kPage > P) {           // the page holds new keys
+                const int pos = lp * kPage + k_row;  // this lane's key
+                if (pos >= P && pos < L) ks = k_new_h + (int64_t)(pos - P) * new_stride + k_chunk;
             }
+            dma16(ks, kdst + pg * kPageBytes + sub * 1024);
+            if (lp * kPage < P) dma16(vpool + base + v_src, vdst + pg * kPageBytes + sub * 1024);
         }
+    };
+    auto page_ids = [&](const int ids, int (&blk)[NI]) {
+#pragma unroll
+        for (int e = 0; e < NI; ++e) blk[e] = __builtin_amdgcn_readlane(ids, page_of(e));
+    };
+    auto issue_tile = [&](unsigned char* kdst, unsigned char* vdst, int kt, const int ids) {
+        int blk[NI];
+        page_ids(ids, blk);
+#pragma unroll
+        for (int e = 0; e < NI; ++e) issue_page(kdst, vdst, kt, blk[e], e);
     };
     // After this wave's loads of tile kt landed: value slots at or past the sequence
     // end become 0 (masked keys get weight 0, and 0 * NaN would poison the product).
@@ -295,7 +310,8 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
 #pragma unroll
     for (int db = 0; db < DB; ++db) o[db] = f32x16{};
     float m_run = -INFINITY;  // max of score * scale * log2(e) used as the exponent offset
-    float l_run = 0.f;        // this lane's half of the row sum of the bf16 weights
+    float l_run = 0.f;        // this lane's half of the row sum of the bf16 weights,
+    float l_run1 = 0.f;       // accumulated in two independent sums
     const float c = a.scale_log2;
     // key row fed to the QK^T product by this lane: bits 2 and 3 of lr swapped
     const int prow = (lr & 0x13) | ((lr & 4) << 1) | ((lr & 8) >> 1);
@@ -304,7 +320,8 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     // LDS fragment reads kept in flight ahead of their MFMA (fewer when 8-bit codes
     // for the next tile occupy registers during the products)
     constexpr int kAhead = ((FP8 || FUSE) && WAVES == 4 && D == 128) ? 4 : 6;
-    auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt) {
+    // hook(i) runs after the i-th QK^T product is issued (the next tile's copies go there)
+    auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt, auto&& hook) {
         // S^T = K_tile . Q^T: MFMA i uses K fragment (k = i/2, block b = i%2). Every
         // group below is fenced so the fragment reads stay kAhead MFMAs ahead.
         bf16x8 kf[2 * DK];
@@ -321,6 +338,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
         for (int i = 0; i < 2 * DK; ++i) {
             if (i + kAhead < 2 * DK) kread(i + kAhead);
             s[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[i >> 1], s[i & 1], 0, 0, 0);
+            hook(i);
             __builtin_amdgcn_sched_barrier(0);
         }
         // V fragments of the first value page go out now; they land during the softmax
@@ -346,11 +364,13 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
         }
         // row maximum: NaN-propagating maxima need no operand canonicalisation and
         // fold three operands per instruction
-        float mx = s[0][0];
+        float mx = s[0][0], mx1 = s[1][0];  // two independent chains
 #pragma unroll
-        for (int e = 1; e < 16; ++e) mx = __builtin_elementwise_maximum(mx, s[0][e]);
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = __builtin_elementwise_maximum(mx, s[1][e]);
+        for (int e = 1; e < 16; ++e) {
+            mx = __builtin_elementwise_maximum(mx, s[0][e]);
+            mx1 = __builtin_elementwise_maximum(mx1, s[1][e]);
+        }
+        mx = __builtin_elementwise_maximum(mx, mx1);
         {
             const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
             mx = __builtin_elementwise_maximum(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
@@ -363,6 +383,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
             const float alpha = m_new == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
+            l_run1 *= alpha;
 #pragma unroll
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
         }
@@ -378,10 +399,14 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
             for (int e = 0; e < 8; ++e)
                 pf[st][e] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[b][e0 + e], c, -m_use));
 #pragma unroll
-            for (int x = 0; x < 4; ++x) {
-                const bf16x2 pair = {pf[st][2 * x], pf[st][2 * x + 1]};
-                l_run = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, l_run, false);
+            for (int x = 0; x < 4; x += 2) {
+                const bf16x2 p0 = {pf[st][2 * x], pf[st][2 * x + 1]};
+                const bf16x2 p1 = {pf[st][2 * x + 2], pf[st][2 * x + 3]};
+                l_run = __builtin_amdgcn_fdot2_f32_bf16(p0, ones, l_run, false);
+                l_run1 = __builtin_amdgcn_fdot2_f32_bf16(p1, ones, l_run1, false);
             }
+            // keep the sums here, beside the products (not sunk to the end of the tile)
+            asm volatile("" : "+v"(l_run), "+v"(l_run1));
         };
         weights(0);
         __builtin_amdgcn_sched_barrier(0);
@@ -535,15 +560,31 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
         const bool more = kt + 1 < it.kt_end;
         int bl_next[4];
         if constexpr (FUSE) take_ids(bl_next);
+        // the next tile's block ids, read before any copy of this step is in flight (the
+        // compiler waits for every outstanding load before reading `ids`)
+        int nb[NI];
+        page_ids(ids, nb);
         if (more) {
-            if constexpr (FP8) load8(kt + 1, ids);
-            else issue_tile(kn, vn, kt + 1, ids);
+            if constexpr (FP8) {
+                load8(kt + 1, ids);
+                if (kt + 2 < it.kt_end) fetch_ids(kt + 2, ids);
+            }
             if constexpr (FUSE)
                 if (has_new(kt + 1)) load_newv(kt + 1);
-            if (kt + 2 < it.kt_end) fetch_ids(kt + 2, ids);
         }
         if constexpr (FUSE) write_own(kc, vc, kt, bl_cur);
-        compute_tile(kc, vc, kt);
+        // bf16 pools: the next tile's copies are issued between the first products of
+        // this one (piece e after product 3e + 1), then the table entries of the tile after
+        static_assert(3 * NI < 2 * DK, "copies fit between the QK^T products");
+        compute_tile(kc, vc, kt, [&](int i) {
+            if constexpr (!FP8) {
+                if (i % 3 == 1 && i / 3 < NI) {
+                    if (more) issue_page(kn, vn, kt + 1, nb[i / 3], i / 3);
+                } else if (i == 3 * NI) {
+                    if (kt + 2 < it.kt_end) fetch_ids(kt + 2, ids);
+                }
+            }
+        });
         if (more) {
             if constexpr (FP8) {
                 store8(kn, vn, kt + 1);
@@ -584,6 +625,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
         if (++kt >= it.kt_end) break;
     }
 
+    l_run += l_run1;
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     const float inv = l_tot > 0.f ? a.v_scale / l_tot : 0.f;  // v_scale is 1 for bf16 pools
     const float lse_v = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
