@@ -278,6 +278,21 @@ gc_status gc_prefix_prefill_prepare_fp8(const gc_geometry* geo, const gc_batch* 
 #define GC_READ_PROBE_SINK_WORDS (2048 * 256)
 gc_status gc_read_bandwidth_probe(const void* buf, size_t bytes, void* sink, hipStream_t stream);
 
+/*
+ * Calibration, not part of the attention path: a register-only loop of
+ * independent bf16 matrix-core products (v_mfma_f32_32x32x16_bf16, 32768 flops
+ * each) on every SIMD: GC_MFMA_PROBE_PRODUCTS_PER_ITERATION products per
+ * iteration over the whole launch. Every operand element is 1; it writes
+ * GC_MFMA_PROBE_SINK_FLOATS floats to `sink` (device), each 4096 * iterations
+ * (exact while that is below 2^24). Timing it gives the sustained bf16 MFMA rate that the
+ * compute-bound attention cases are also reported against (the nominal 2.5
+ * PFLOP/s assumes the peak clock). iterations < 0: GC_ERR_BAD_SHAPE;
+ * iterations == 0: GC_OK, nothing enqueued.
+ */
+#define GC_MFMA_PROBE_SINK_FLOATS (1024 * 256)
+#define GC_MFMA_PROBE_PRODUCTS_PER_ITERATION (1024 * 4 * 16)
+gc_status gc_mfma_peak_probe(int32_t iterations, void* sink, hipStream_t stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* gc_status_string(gc_status status);
 

@@ -26,8 +26,11 @@ EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefi
             "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_kv_append_fp8",
             "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_prefix_prefill_prepare",
             "gc_prefix_prefill_prepare_fp8", "gc_prefix_prefill_run_with_append", "gc_read_bandwidth_probe",
-            "gc_status_string")
+            "gc_mfma_peak_probe", "gc_status_string")
 READ_PROBE_SINK_WORDS = 2048 * 256
+MFMA_PROBE_SINK_FLOATS = 1024 * 256
+MFMA_PROBE_PRODUCTS_PER_ITERATION = 1024 * 4 * 16
+MFMA_PROBE_FLOPS_PER_PRODUCT = 32 * 32 * 16 * 2
 
 
 class GcError(RuntimeError):
@@ -104,6 +107,8 @@ def load_library(path: str | None = None):
                                                       ctypes.c_size_t, vp]
     lib.gc_read_bandwidth_probe.restype = i32
     lib.gc_read_bandwidth_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
+    lib.gc_mfma_peak_probe.restype = i32
+    lib.gc_mfma_peak_probe.argtypes = [i32, vp, vp]
     lib.gc_status_string.restype = ctypes.c_char_p
     lib.gc_status_string.argtypes = [i32]
     if path is None:
@@ -346,6 +351,22 @@ def read_bandwidth_probe(buf, sink=None, stream=None):
     st = lib.gc_read_bandwidth_probe(buf.data_ptr(), buf.numel() * buf.element_size(), sink.data_ptr(),
                                      _stream_handle(stream))
     _check("gc_read_bandwidth_probe", st, lib)
+    return sink
+
+
+def mfma_peak_probe(iterations, sink=None, device=None, stream=None):
+    """Enqueue the matrix-core calibration loop (`iterations` rounds of
+    MFMA_PROBE_PRODUCTS_PER_ITERATION bf16 32x32x16 products); returns the sink
+    tensor it writes (every entry 4096 * iterations)."""
+    import torch
+    lib = load_library()
+    if sink is None:
+        sink = torch.empty(MFMA_PROBE_SINK_FLOATS, dtype=torch.float32, device=device or "cuda")
+    _require(sink, torch.float32, "sink")
+    if sink.numel() < MFMA_PROBE_SINK_FLOATS:
+        raise ValueError(f"sink needs {MFMA_PROBE_SINK_FLOATS} floats")
+    st = lib.gc_mfma_peak_probe(int(iterations), sink.data_ptr(), _stream_handle(stream))
+    _check("gc_mfma_peak_probe", st, lib)
     return sink
 
 

@@ -546,6 +546,18 @@ gc_status gc_read_bandwidth_probe(const void* buf, size_t bytes, void* sink, hip
 }
 
 __attribute__((visibility("default")))
+gc_status gc_mfma_peak_probe(int32_t iterations, void* sink, hipStream_t stream) {
+    static_assert(GC_MFMA_PROBE_SINK_FLOATS == gc::kMfmaProbeBlocks * gc::kProbeThreads, "sink size");
+    static_assert(GC_MFMA_PROBE_PRODUCTS_PER_ITERATION ==
+                      gc::kMfmaProbeBlocks * (gc::kProbeThreads / 64) * gc::kMfmaProbeChains * gc::kMfmaProbePerChain,
+                  "products per iteration");
+    if (sink == nullptr) return GC_ERR_NULL_ARG;
+    if (iterations < 0) return GC_ERR_BAD_SHAPE;
+    if (iterations == 0) return GC_OK;
+    return gc::launch_mfma_probe(iterations, static_cast<float*>(sink), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+}
+
+__attribute__((visibility("default")))
 const char* gc_status_string(gc_status s) {
     switch (s) {
         case GC_OK: return "GC_OK: success";

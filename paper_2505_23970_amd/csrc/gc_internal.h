@@ -32,6 +32,9 @@ constexpr int kCombineThreads = 256;  // threads per split-merge workgroup
 constexpr int kPlanLdsBatch = 2048;   // batches up to this size are planned from LDS copies
 constexpr int kProbeBlocks = 2048;    // read-probe grid
 constexpr int kProbeThreads = 256;
+constexpr int kMfmaProbeBlocks = 1024;   // matrix-core probe grid: four workgroups per CU
+constexpr int kMfmaProbeChains = 4;      // independent accumulators per wavefront
+constexpr int kMfmaProbePerChain = 4;    // products per accumulator per iteration
 
 // One attention work item: query tile [q0, q0 + tq) of request r against key
 // tiles [kt_begin, kt_end). part >= 0 marks a split item whose normalised
@@ -193,6 +196,7 @@ hipError_t launch_attention_append(const AttnArgs& a, int head_dim, int64_t num_
 hipError_t launch_attention_small(const AttnArgs& a, int head_dim, int64_t num_items, bool fp8,
                                   hipStream_t s);
 hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);
+hipError_t launch_mfma_probe(int iterations, float* sink, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, int head_dim, int64_t num_combines, hipStream_t s);
 
 }  // namespace gc

@@ -40,6 +40,12 @@ def test_read_probe_rejects_bad_arguments(lib):
     assert lib.gc_read_bandwidth_probe(0x2000, 0, 0x2000, None) == 0       # nothing to read, nothing enqueued
 
 
+def test_mfma_probe_rejects_bad_arguments(lib):
+    assert lib.gc_mfma_peak_probe(10, None, None) == -1
+    assert lib.gc_mfma_peak_probe(-1, 0x2000, None) == -2
+    assert lib.gc_mfma_peak_probe(0, 0x2000, None) == 0       # nothing to run, nothing enqueued
+
+
 def test_status_strings(lib):
     for code, name in gc.STATUS_NAMES.items():
         assert lib.gc_status_string(code).decode().startswith(name)

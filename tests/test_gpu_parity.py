@@ -323,6 +323,19 @@ def test_read_probe_reads_every_word():
     assert len(nz) == 1 and int(sink[nz[0]].item()) == 0x5A5A
 
 
+def test_mfma_probe_runs_every_product():
+    """The matrix-core calibration loop multiplies all-ones operands: every product adds
+    16 to each of a thread's 4 x 16 accumulator elements, 4 products per accumulator
+    per iteration, so every sink entry is exactly 4096 * iterations; a dropped or
+    duplicated product changes it."""
+    import torch
+    import paper_2505_23970_amd as gc
+    for it in (1, 37, 100):
+        sink = gc.mfma_peak_probe(it)
+        torch.cuda.synchronize()
+        assert torch.all(sink == 4096.0 * it).item()
+
+
 @pytest.mark.parametrize("source", ["pinned_host", "device"])
 def test_restore_prefix_from_host_tier(source):
     """Restoring every cached prefix into an all-NaN pool (positions 0 .. P_r - 1 written
