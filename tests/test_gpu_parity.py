@@ -250,6 +250,64 @@ def test_block_relabelling_is_bitwise_invisible():
     assert np.array_equal(H.from_dev_f32(l1), H.from_dev_f32(l2))
 
 
+@pytest.mark.parametrize("kv,tiling", [("bf16", "prefill"), ("bf16", "wide"), ("bf16", "small"),
+                                       ("bf16", "fused"), ("fp8", "prefill"), ("fp8", "small")])
+def test_pool_beyond_4_gib(kv, tiling):
+    """Block ids whose byte offsets exceed 2^32: the same batch run on its own pool and
+    with every block id shifted past 4 GiB inside a larger pool gives bitwise the same
+    output, LSE and appended pages ("fused": the shifted run appends inside the
+    attention launch). The blocks that a 32-bit wraparound of those offsets would
+    land on hold NaN, so a truncated offset shows up."""
+    import torch
+    import paper_2505_23970_amd as gc
+    til = {"prefill": gc.TILES_PREFILL, "wide": gc.TILES_WIDE, "small": gc.TILES_SMALL,
+           "fused": gc.TILES_PREFILL}[tiling]
+    w = W.build([300, 17, 96], [37, 5, 64], 16, 2, 128, seed=330, values="unit")
+    say(f"case pool beyond 4 GiB: kv={kv} tiling={tiling}")
+    fp8 = kv == "fp8"
+    ks, vs = 2.0 ** -6, 0.0213
+    ref = H.DeviceRunFp8(w, ks, vs) if fp8 else H.DeviceRun(w)
+    ref.append()
+    o1, l1 = ref.attention(tiling=til)
+    NB = w.num_blocks
+    page_bytes = w.num_kv_heads * 16 * w.head_dim * (1 if fp8 else 2)
+    shift = (1 << 32) // page_bytes
+    dtype = torch.uint8 if fp8 else torch.bfloat16
+    nan = 0x7F if fp8 else int(W.BF16_NAN)
+    pools = []
+    for small in (ref.k_pool, ref.v_pool):
+        big = torch.empty((shift + NB,) + tuple(small.shape[1:]), dtype=dtype, device="cuda")
+        (big[:NB] if fp8 else big[:NB].view(torch.int16)).fill_(nan)
+        pools.append(big)
+    init_k = H.to_dev_u8(ref.k8_init) if fp8 else H.to_dev_bf16(w.k_pool)
+    init_v = H.to_dev_u8(ref.v8_init) if fp8 else H.to_dev_bf16(w.v_pool)
+    pools[0][shift:] = init_k
+    pools[1][shift:] = init_v
+    batch = gc.PagedBatch(w.prefix_lens, w.new_lens, (w.block_tables + shift).astype(np.int32))
+    T, Hq, D = w.q.shape
+    o2 = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    l2 = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    if fp8:
+        gc.kv_append_fp8(ref.k_new, ref.v_new, pools[0], pools[1], batch, ks, vs)
+        gc.prefix_prefill_attention_fp8(ref.q, pools[0], pools[1], batch, w.scale, ks, vs, out=o2, lse=l2,
+                                        tiling=til)
+    elif tiling == "fused":
+        shifted = H.DeviceRun.__new__(H.DeviceRun)
+        shifted.w, shifted.batch, shifted.k_pool, shifted.v_pool = w, batch, pools[0], pools[1]
+        shifted.q, shifted.k_new, shifted.v_new = ref.q, ref.k_new, ref.v_new
+        o2, l2 = fused_run(shifted, tiling=til)
+    else:
+        gc.kv_append(ref.k_new, ref.v_new, pools[0], pools[1], batch)
+        gc.prefix_prefill_attention(ref.q, pools[0], pools[1], batch, w.scale, out=o2, lse=l2, tiling=til)
+    torch.cuda.synchronize()
+    assert np.array_equal(H.from_dev_bits(o1), H.from_dev_bits(o2))
+    assert np.array_equal(H.from_dev_f32(l1), H.from_dev_f32(l2))
+    for big, small in zip(pools, (ref.k_pool, ref.v_pool)):
+        assert torch.equal(big[shift:].view(torch.uint8), small.view(torch.uint8))
+    del pools
+    torch.cuda.empty_cache()
+
+
 def test_plan_once_run_twice():
     import torch
     import paper_2505_23970_amd as gc
