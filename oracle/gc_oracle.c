@@ -17,8 +17,11 @@
  *   the result must equal a full recomputation over prefix + new tokens.
  *   §2.1 "LLM Serving Process": serving is Transformer-based and the prefill
  *   phase processes the whole prompt. The paper never writes the attention
- *   formula, so the textbook causal scaled-dot-product attention is used
- *   (readings listed in the design doc): for new token i of request r (logical
+ *   formula, so the textbook causal scaled-dot-product attention is used (a
+ *   reading, not a statement of the paper: consecutive query heads share a KV
+ *   head, the cached prefix is fully visible, a new token sees itself and the
+ *   new tokens before it; the scale is a caller argument): for new token i of
+ *   request r (logical
  *   position P_r + i) and query head h with KV head kvh = h / (Hq / Hkv),
  *       x_j = scale * <q, k_j>            for j = 0 .. P_r + i (inclusive)
  *       m = max_j x_j,  w_j = exp(x_j - m),  l = sum_j w_j
