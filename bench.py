@@ -33,6 +33,8 @@ METRIC = "prefix-cached prefill attn TFLOP/s + new tokens/s; % of bf16 MFMA/HBM 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 SAMPLE_EVERY = 5            # timed steps per step that carries timing events
+COLD_STEPS = 10             # steps of the cold-cache pass after the timed region
+COLD_FLUSH_MIB = 512        # scratch overwritten before each of them
 
 WORKLOADS = {
     "tiny": lambda: _cfg(1),
@@ -429,6 +431,20 @@ def main():
         step(e)
     torch.cuda.synchronize()
     prep = np.array([e[0].elapsed_time(e[1]) for e in pev])
+    # cold caches: before each of a few steps, stream-read a scratch buffer twice the
+    # size of the 256 MB infinity cache (and of the L2s), so the step reads K/V from HBM
+    # as a layer of a real model would (its K/V evicted by the other layers in between);
+    # a read, not a write, so that no dirty lines are written back during the step. The
+    # events bracket the attention launch only.
+    scratch = torch.ones(COLD_FLUSH_MIB << 20, dtype=torch.uint8, device=dev)
+    sink = gc.read_bandwidth_probe(scratch)
+    cev = [[None] + [torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(COLD_STEPS)]
+    for e in cev:
+        gc.read_bandwidth_probe(scratch, sink)
+        step(e)
+    torch.cuda.synchronize()
+    cold = np.array([e[1].elapsed_time(e[2]) for e in cev])
+    del scratch, sink
     t_att = float(np.mean(att)) * 1e-3
 
     achieved = F / t_att / 1e12
@@ -474,13 +490,17 @@ def main():
                       "append_and_plan": float(np.mean(prep)),
                       "attention": float(np.mean(att)),
                       "attention_p10": float(np.percentile(att, 10)),
-                      "attention_p90": float(np.percentile(att, 90))},
+                      "attention_p90": float(np.percentile(att, 90)),
+                      "attention_cold": float(np.mean(cold)),
+                      "cold_note": f"attention launch after stream-reading {COLD_FLUSH_MIB} MiB (infinity cache "
+                                   f"and L2 evicted), {COLD_STEPS} steps after the timed region"},
         "algorithmic": {"flops": F, "attn_bytes": A, "append_bytes": w.append_bytes()},
         "roofline": {**roof,
                      "traffic": profiled_traffic(w.name + ("_fp8" if fp8 else "")),
                      "kernel": kernel_name,
                      "arithmetic_intensity": F / A,
                      "mfma_frac": achieved / PEAK_BF16_TFLOPS,
+                     "cold_tflops": F / (float(np.mean(cold)) * 1e-3) / 1e12,
                      "hbm_gbs_algorithmic": A / t_att / 1e9},
     }
     if args.cpu_seconds > 0:
