@@ -622,3 +622,28 @@ def test_fused_append_against_the_oracle(split):
     ref_out, ref_lse = H.oracle_rows(w, kp_ref, vp_ref)
     info = H.compare_attention(w, out, lse, ref_out, ref_lse, contract=True)
     say(f"fused vs oracle: {info}")
+
+
+def test_bench_line_keeps_the_contract():
+    """bench.py on the tiny workload prints one JSON line with the contract's fields, the
+    roofline object (measured live) and the CPU-oracle baseline."""
+    import json
+    import os
+    import subprocess
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    res = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--workload", "tiny", "--steps", "5",
+                          "--warmup", "5", "--cpu-seconds", "0.5"], capture_output=True, text=True, timeout=300)
+    assert res.returncode == 0, res.stderr[-2000:]
+    lines = [l for l in res.stdout.splitlines() if l.startswith("{")]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline", "cpu_baseline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 5 and d["warmup"] == 5 and d["config"]["workload"] == "tiny"
+    assert d["value"] > 0 and d["ms_per_step"] > 0 and d["kernel_ms"]["attention_cold"] > 0
+    r = d["roofline"]
+    assert r["bound"] in ("mfma", "hbm") and r["peak"] in (2500.0, 8000.0)
+    assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-9 and r["frac_of_measured"] > 0
+    c = d["cpu_baseline"]
+    assert c["kind"] == "oracle" and c["value"] > 0 and c["cores"] >= 1 and c["sample"]
