@@ -325,6 +325,54 @@ def test_plan_once_run_twice():
     H.compare_attention(w, o1, None, ref, None)
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_small_tile_splits_repeat_on_one_workspace(kv):
+    """Small tiles with key splits (partials and their merge in the workspace), one
+    plan and three runs (q, -q, q) on the same workspace: every run matches the
+    oracle (nothing a run leaves in the workspace leaks into the next), and the
+    first and third are bitwise equal."""
+    import copy
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build([3000, 700, 40, 1500, 2047], [1, 2, 1, 3, 1], 16, 2, 128, seed=304)
+    wn = copy.copy(w)
+    wn.q = (w.q.view(np.uint16) ^ np.uint16(0x8000)).view(w.q.dtype)  # exact negation of bf16
+    til, split = gc.TILES_SMALL, 4
+    T, Hq, D = w.q.shape
+    if kv == "bf16":
+        run = H.DeviceRun(w)
+        run.append()
+        kp, vp = H.oracle_pools(w)
+        refs = [H.oracle_rows(x, kp, vp) for x in (w, wn)]
+        go = gc.run
+        extra = {}
+    else:
+        ks, vs = 0.02, 0.015
+        run = H.DeviceRunFp8(w, ks, vs)
+        run.append()
+        kp8, vp8 = H.oracle_pools_fp8(run)
+        refs = [H.oracle.attention_e4m3(w.prefix_lens, w.new_lens, w.block_tables, w.num_blocks, x.q,
+                                        kp8, vp8, ks, vs, w.scale) for x in (w, wn)]
+        go = gc.run_fp8
+        extra = {"k_scale": ks, "v_scale": vs}
+    say(f"small-tile splits repeat kv={kv} lens={list(w.prefix_lens)}/{list(w.new_lens)} split={split}")
+    ws = gc.alloc_workspace(w.num_q_heads, run.k_pool, run.v_pool, run.batch, kv_split_tiles=split, tiling=til)
+    gc.plan(w.num_q_heads, run.k_pool, run.v_pool, run.batch, ws, kv_split_tiles=split, tiling=til)
+    qn = H.to_dev_bf16(wn.q)
+    outs = []
+    for q, ref in ((run.q, refs[0]), (qn, refs[1]), (run.q, refs[0])):
+        out = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+        go(q, run.k_pool, run.v_pool, run.batch, w.scale, workspace=ws, out=out, lse=lse,
+           kv_split_tiles=split, tiling=til, **extra)
+        torch.cuda.synchronize()
+        H.compare_attention(w, out, lse, ref[0], ref[1],
+                            vmax=None if kv == "bf16" else H.e4m3_vmax(vp8, vs))
+        outs.append((H.from_dev_bits(out), H.from_dev_f32(lse)))
+    assert np.array_equal(outs[0][0], outs[2][0]) and np.array_equal(outs[0][1], outs[2][1])
+
+
+
 def test_two_turns_equal_one_call():
     """Multi-turn reuse: turn 1 appends n1 tokens and attends; turn 2 treats them as
     cached prefix. The rows match a single call over n1 + n2 new tokens."""
