@@ -74,10 +74,11 @@ struct SmallFrags<D, false> {
 };
 template <int D>
 struct SmallFrags<D, true> {
-    u32x2 k[2][D / 32];      // 8 codes
+    u32x4 k[2][D / 64];      // 16 codes: the K^T operands of k-steps 2p and 2p + 1
     uint32_t v[2][D / 16];   // 4 codes
     __device__ __forceinline__ bf16x8 kop(int b, int s) const {
-        const u32x2 a = widen_e4m3x4(k[b][s][0]), c = widen_e4m3x4(k[b][s][1]);
+        const u32x4 w = k[b][s >> 1];
+        const u32x2 a = widen_e4m3x4(w[2 * (s & 1)]), c = widen_e4m3x4(w[2 * (s & 1) + 1]);
         return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], c[0], c[1]});
     }
     __device__ __forceinline__ u32x2 vop(int b, int db) const { return widen_e4m3x4(v[b][db]); }
@@ -113,12 +114,17 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
     const int lim = P + it.q0 + (row_ok ? t : 0);  // last key this row may see
     const int64_t qrow = (int64_t)(cu + it.q0 + t) * a.num_q_heads + kvh * a.group + hl;
 
-    // Q^T operand of k-step s: lane holds q[row j][32 s + 8 g4 .. +7]
+    // Q^T operand of k-step s: lane holds q[row j][32 s + 8 g4 .. +7]. Over 8-bit
+    // pools the head dimension is taken in another order (the sum over d does not
+    // depend on it): k-steps 2p and 2p + 1 cover d = 64 p + 16 g4 .. +15 of lane
+    // group g4, so one 16-byte load brings a lane's K codes for both steps.
     bf16x8 qf[KS];
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-        qf[s] = row_ok ? *reinterpret_cast<const bf16x8*>(a.q + qrow * D + 32 * s + 8 * g4)
+    for (int s = 0; s < KS; ++s) {
+        const int d0 = FP8 ? 64 * (s >> 1) + 16 * g4 + 8 * (s & 1) : 32 * s + 8 * g4;
+        qf[s] = row_ok ? *reinterpret_cast<const bf16x8*>(a.q + qrow * D + d0)
                        : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
 
     // Score block b holds the 16 keys of page b of the tile (operand row i = key
     // slot i), so accumulator value v of block b is key 16 b + 4 g4 + v. The P^T
@@ -132,7 +138,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
     const int64_t block_bytes = (int64_t)a.num_kv_heads * page_bytes;
     const unsigned char* kbase = reinterpret_cast<const unsigned char*>(a.k_pool) + (int64_t)kvh * page_bytes;
     const unsigned char* vbase = reinterpret_cast<const unsigned char*>(a.v_pool) + (int64_t)kvh * page_bytes;
-    const uint32_t k_off = (uint32_t)(j * D + 8 * g4) * EB;         // + 32 EB s bytes per k-step
+    const uint32_t k_off = (uint32_t)(j * D + (FP8 ? 16 : 8) * g4) * EB;  // + 64 B per k-step (pair)
     const uint32_t v_off = (uint32_t)(j * kPage + 4 * g4) * EB;     // + 256 EB db bytes per value block
 
     using Frags = SmallFrags<D, FP8>;
@@ -164,8 +170,8 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
                 (void*)(vbase + blk[b] * block_bytes), (short)0, (int)page_bytes, kBufferFlags);
             if constexpr (FP8) {
 #pragma unroll
-                for (int s = 0; s < KS; ++s)
-                    f.k[b][s] = __builtin_amdgcn_raw_buffer_load_b64(kr, (int)k_off + 32 * s, 0, 0);
+                for (int p = 0; p < KS / 2; ++p)
+                    f.k[b][p] = __builtin_amdgcn_raw_buffer_load_b128(kr, (int)k_off + 64 * p, 0, 0);
 #pragma unroll
                 for (int db = 0; db < DB; ++db)
                     f.v[b][db] = __builtin_amdgcn_raw_buffer_load_b32(vr, (int)v_off + 256 * db, 0, 0);
@@ -254,28 +260,46 @@ __global__ __launch_bounds__(kDecWaves * 64, 1) void attention_small_kernel(cons
         }
     };
 
-    // Three fragment sets used in turn (no register copies): the loads of tiles kt+1
-    // and kt+2 are in flight while tile kt is computed. Loads are issued
+    // NS fragment sets used in turn (no register copies): the loads of tiles kt+1 ..
+    // kt+NS-1 are in flight while tile kt is computed. Loads are issued
     // unconditionally (past the last tile the last tile is loaded again), so the
     // compiler's wait before a tile's products covers exactly that tile's loads.
-    Frags f0, f1, f2;
+    // 8-bit tiles take 20 loads per lane, so three tiles ahead stay within the
+    // 63 loads the vector-memory counter can track; bf16 tiles (24 loads, twice
+    // the registers) keep two.
+    constexpr int NS = FP8 ? 4 : 3;
+    Frags f0, f1, f2, f3;
     const int kt_end = it.kt_end, last = kt_end - 1;
     int kt = it.kt_begin;
     load(kt, fetch_ids(kt), f0);
     load(min(kt + 1, last), fetch_ids(min(kt + 1, last)), f1);
-    Ids ids = fetch_ids(min(kt + 2, last));
-    auto step = [&](Frags& cur, Frags& ahead2) {
-        load(min(kt + 2, last), ids, ahead2);
-        ids = fetch_ids(min(kt + 3, last));
+    if constexpr (NS == 4) load(min(kt + 2, last), fetch_ids(min(kt + 2, last)), f2);
+    Ids ids = fetch_ids(min(kt + NS - 1, last));
+    auto step = [&](Frags& cur, Frags& ahead) {
+        load(min(kt + NS - 1, last), ids, ahead);
+        ids = fetch_ids(min(kt + NS, last));
         compute(kt, cur);
     };
-    while (true) {
-        step(f0, f2);
-        if (++kt >= kt_end) break;
-        step(f1, f0);
-        if (++kt >= kt_end) break;
-        step(f2, f1);
-        if (++kt >= kt_end) break;
+    if constexpr (NS == 3) {
+        while (true) {
+            step(f0, f2);
+            if (++kt >= kt_end) break;
+            step(f1, f0);
+            if (++kt >= kt_end) break;
+            step(f2, f1);
+            if (++kt >= kt_end) break;
+        }
+    } else {
+        while (true) {
+            step(f0, f3);
+            if (++kt >= kt_end) break;
+            step(f1, f0);
+            if (++kt >= kt_end) break;
+            step(f2, f1);
+            if (++kt >= kt_end) break;
+            step(f3, f2);
+            if (++kt >= kt_end) break;
+        }
     }
 
     const float l_tot = row_sum4(l_run);
