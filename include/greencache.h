@@ -65,7 +65,9 @@ typedef enum gc_status {
                                 small tiles forced with Hq/Hkv > 16 */
     GC_ERR_BLOCK_TABLE = -4, /* ceil((P_r + n_r) / page_size) > max_blocks_per_seq */
     GC_ERR_WORKSPACE = -5,   /* workspace NULL or smaller than required */
-    GC_ERR_HIP = -6          /* a HIP launch or runtime call failed */
+    GC_ERR_HIP = -6,         /* a HIP launch or runtime call failed */
+    GC_ERR_LENGTHS = -7      /* the device length arrays disagree with the host's
+                                (reported by gc_prefix_prefill_plan_status) */
 } gc_status;
 
 /* Model and pool geometry. */
@@ -147,6 +149,27 @@ gc_status gc_prefix_prefill_workspace_size(const gc_geometry* geo, const gc_batc
 gc_status gc_prefix_prefill_plan(const gc_geometry* geo, const gc_batch* batch,
                                  const gc_plan_options* opts,
                                  void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Whether the last plan written into `workspace` (by gc_prefix_prefill_plan,
+ * gc_prefix_prefill_attention[_fp8] or gc_prefix_prefill_prepare[_fp8]) was
+ * built from device lengths that agree with the host's. The planner checks on
+ * the device that cu_new_lens_dev starts at 0, never decreases and ends at the
+ * host's T, that every prefix_lens_dev entry is >= 0, that every request's
+ * keys fit its block-table row, and that the work-item, merge and partial
+ * counts equal those the host derived from the host lengths. When any check
+ * fails the plan holds no work: a run on it enqueues kernels that write nothing
+ * (out and lse keep their contents), and nothing is accessed out of bounds.
+ * The check result is an int32 at byte offset 0 of the workspace (0: agree,
+ * 1: disagree). This call waits for `stream` (the plan must have been enqueued
+ * on it), reads that word and returns GC_OK or GC_ERR_LENGTHS; GC_ERR_NULL_ARG
+ * for a NULL workspace, GC_ERR_WORKSPACE for workspace_bytes < 4, GC_ERR_HIP if
+ * the copy or the wait fails. It is the one entry point that blocks the host.
+ * (§2.2: the caller owns the lookup that produces the lengths; the library
+ * rejects a batch whose two copies disagree, visibly.)
+ */
+gc_status gc_prefix_prefill_plan_status(const void* workspace, size_t workspace_bytes,
+                                        hipStream_t stream);
 
 /*
  * Attention of the new tokens over the cached prefix plus the new tokens

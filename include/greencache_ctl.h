@@ -5,8 +5,8 @@
  * a size-limited cache and evicts, when space is needed or the cache shrinks,
  * the entries with the lowest score (§5.5 "Cache Manager and Replacement
  * Policy"). This library replays a request trace through such a cache under
- * one of the policies the paper compares (§6.5, "Replacement Policy
- * Comparison"): FIFO, LRU and Least Carbon Savings (LCS, Eq. 7, with the
+ * one of the policies the paper compares (§6.3.2, "Replacement Policy
+ * Comparison", Table tab:replacement): FIFO, LRU and Least Carbon Savings (LCS, Eq. 7, with the
  * multi-turn form of Eq. 8; the document form of Eq. 9 coincides with Eq. 7
  * here, see gc_policy). It holds no GPU code.
  *
@@ -33,7 +33,7 @@
  *     with size in bytes and age = max(now - insertion time, 1e-6) seconds;
  *     products and quotients in IEEE double in exactly this order.
  *   - Requests must come in non-decreasing time order.
- * Token hit rate (the paper's "cache hit rate", §6.5) = reused tokens / sum
+ * Token hit rate (the paper's "cache hit rate", §6.3.2) = reused tokens / sum
  * of prompt_tokens.
  *
  * Conventions: all pointers belong to the caller; a gc_cache is not

@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE. Only tests/ and the benchmark's CPU-baseline leg may
 import this module. The product (paper_2505_23970_amd/control.py and
 csrc/cache_policy.cpp) shares no code with it.
 
-Carbon model, GreenCache §3.1 (Eqs. 1-5):
+Carbon model, GreenCache §2.3 (Eqs. 1-3) and §3.2.1 (Eqs. 4-5):
   total carbon C = C_o + (T / LT) * C_e                         (Eq. 1)
   operational C_o = E * CI                                       (Eq. 2)
   embodied C_e = sum over GPU, CPU, memory, SSD                  (Eq. 3)
@@ -15,12 +15,12 @@ Units here: energy in kWh, CI in gCO2e/kWh, embodied carbon in kgCO2e
 (converted to grams), times in hours, lifetimes in years (365 days).
 
 Replacement policies, §5.5 (Eq. 7 LCS score, Eq. 8 multi-turn form) and the
-FIFO / LRU baselines of §6.5, on the cache model stated in
+FIFO / LRU baselines of §6.3.2 (Table tab:replacement), on the cache model stated in
 include/greencache_ctl.h (the model is a reading: the paper states the score,
 not the bookkeeping). Each eviction sorts every candidate entry by
 (score, insertion time, key) and removes the first: slow and obviously right.
 
-Cache-size ILP, §5.4 Eq. 6, with one cache size per time step chosen from a
+Cache-size ILP, §5.4.1 Eq. 6, with one cache size per time step chosen from a
 discrete set: minimise the summed per-request carbon subject to at least
 rho * N requests meeting the TTFT SLO and at least rho * N meeting the TPOT
 SLO. Solved here by enumerating every assignment (tiny instances only).

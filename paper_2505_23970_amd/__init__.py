@@ -20,12 +20,14 @@ LIBRARY = os.path.join(_HERE, "libgreencache.so")
 
 GC_OK = 0
 STATUS_NAMES = {0: "GC_OK", -1: "GC_ERR_NULL_ARG", -2: "GC_ERR_BAD_SHAPE", -3: "GC_ERR_UNSUPPORTED",
-                -4: "GC_ERR_BLOCK_TABLE", -5: "GC_ERR_WORKSPACE", -6: "GC_ERR_HIP"}
+                -4: "GC_ERR_BLOCK_TABLE", -5: "GC_ERR_WORKSPACE", -6: "GC_ERR_HIP", -7: "GC_ERR_LENGTHS"}
+GC_ERR_LENGTHS = -7
 
 EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefill_plan",
             "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_kv_append_fp8",
             "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_prefix_prefill_prepare",
-            "gc_prefix_prefill_prepare_fp8", "gc_prefix_prefill_run_with_append", "gc_read_bandwidth_probe",
+            "gc_prefix_prefill_prepare_fp8", "gc_prefix_prefill_run_with_append",
+            "gc_prefix_prefill_plan_status", "gc_read_bandwidth_probe",
             "gc_mfma_peak_probe", "gc_status_string")
 READ_PROBE_SINK_WORDS = 2048 * 256
 MFMA_PROBE_SINK_FLOATS = 1024 * 256
@@ -105,6 +107,8 @@ def load_library(path: str | None = None):
     lib.gc_prefix_prefill_run_with_append.restype = i32
     lib.gc_prefix_prefill_run_with_append.argtypes = [G, Bp, O, vp, vp, vp, vp, vp, f32, vp, vp, vp,
                                                       ctypes.c_size_t, vp]
+    lib.gc_prefix_prefill_plan_status.restype = i32
+    lib.gc_prefix_prefill_plan_status.argtypes = [vp, ctypes.c_size_t, vp]
     lib.gc_read_bandwidth_probe.restype = i32
     lib.gc_read_bandwidth_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
     lib.gc_mfma_peak_probe.restype = i32
@@ -290,7 +294,8 @@ def _attn_args(q, k_pool, v_pool, batch, out, lse, workspace, pool_dtype=None):
         _require(lse, torch.float32, "lse", batch.device)
         if tuple(lse.shape) != (T, Hq):
             raise ValueError("lse must be [T][Hq] float32")
-    _require(workspace, torch.uint8, "workspace", batch.device)
+    if workspace is not None:
+        _require(workspace, torch.uint8, "workspace", batch.device)
     return geo, out
 
 
@@ -304,6 +309,19 @@ def plan(num_q_heads, k_pool, v_pool, batch: PagedBatch, workspace, kv_split_til
                                     _opts(kv_split_tiles, tiling), workspace.data_ptr(),
                                     workspace.numel(), _stream_handle(stream))
     _check("gc_prefix_prefill_plan", st, lib)
+
+
+def plan_status(workspace, stream=None) -> int:
+    """Status of the last plan in `workspace` (waits for the stream): GC_OK when the
+    device lengths agreed with the host's, GC_ERR_LENGTHS when they did not (the plan
+    then holds no work). Other failures raise."""
+    import torch
+    lib = load_library()
+    _require(workspace, torch.uint8, "workspace")
+    st = lib.gc_prefix_prefill_plan_status(workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    if st not in (GC_OK, GC_ERR_LENGTHS):
+        _check("gc_prefix_prefill_plan_status", st, lib)
+    return int(st)
 
 
 def run(q, k_pool, v_pool, batch: PagedBatch, scale, workspace, out=None, lse=None,

@@ -2,10 +2,10 @@
 model (native library libgreencache_ctl.so, C ABI in include/greencache_ctl.h)
 and the hourly cache-size ILP.
 
-GreenCache §3.1 (Eqs. 1-5) prices a serving interval as operational carbon
+GreenCache §2.3 (Eqs. 1-3) and §3.2.1 (Eqs. 4-5) price a serving interval as operational carbon
 (energy x grid carbon intensity) plus the amortised embodied carbon of the
 platform, with the cache's SSD share proportional to the allocated capacity.
-§5.4 (Eq. 6) picks, per decision interval, the cache size that minimises the
+§5.4.1 (Eq. 6) picks, per decision interval, the cache size that minimises the
 summed per-request carbon while at least rho of all requests meet the TTFT SLO
 and at least rho meet the TPOT SLO; the paper solves it with an ILP solver
 (PuLP + CBC), here scipy's HiGHS interface. §5.5 (Eqs. 7-8) evicts the
@@ -119,7 +119,7 @@ class Cache:
 
 
 def token_hit_rate(policy: str, capacity_bytes: int, bytes_per_token: int, trace: np.ndarray) -> float:
-    """The paper's cache hit rate (§6.5): reused tokens over all input tokens."""
+    """The paper's cache hit rate (§6.3.2, Table tab:replacement): reused tokens over all input tokens."""
     c = Cache(policy, capacity_bytes, bytes_per_token)
     reused = c.replay(trace)
     return float(reused.sum()) / float(np.sum(trace["prompt_tokens"]))
@@ -130,7 +130,7 @@ def token_hit_rate(policy: str, capacity_bytes: int, bytes_per_token: int, trace
 @dataclasses.dataclass(frozen=True)
 class Platform:
     """Embodied carbon of the serving platform (Table 1) and component lifetimes
-    (5 years, §3.1). The SSD's embodied carbon is per allocated TB."""
+    (5 years, §2.3). The SSD's embodied carbon is per allocated TB."""
     gpu_kg: float = 106.4
     cpu_kg: float = 9.3
     mem_kg: float = 30.8

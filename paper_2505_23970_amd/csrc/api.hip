@@ -60,6 +60,11 @@ gc_status check_common(const gc_geometry* geo, const gc_batch* b, Shape* sh) {
             return GC_ERR_BLOCK_TABLE;
     }
     sh->total_tokens = total;
+    // the append grid: one workgroup per (page receiving new tokens, KV head), plus
+    // the planner's in the combined launch
+    if (gc::append_pages_host(b->prefix_lens_host, b->new_lens_host, b->batch) * geo->num_kv_heads >=
+        (int64_t)INT32_MAX)
+        return GC_ERR_UNSUPPORTED;
     if (total > 0) {
         if (geo->num_blocks <= 0) return GC_ERR_BAD_SHAPE;
         if (b->prefix_lens_dev == nullptr || b->cu_new_lens_dev == nullptr ||
@@ -203,7 +208,7 @@ gc_status plan_checked(const gc_geometry* geo, const gc_batch* b, const gc_plan_
     return make_plan(geo, b, *sh, o, pl);
 }
 
-gc::PlanArgs plan_args(const gc_batch* b, const Shape& sh, const Plan& pl, void* ws) {
+gc::PlanArgs plan_args(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl, void* ws) {
     gc::PlanArgs a{};
     a.prefix_lens = b->prefix_lens_dev;
     a.cu_new_lens = b->cu_new_lens_dev;
@@ -221,13 +226,14 @@ gc::PlanArgs plan_args(const gc_batch* b, const Shape& sh, const Plan& pl, void*
     a.expect_items = (int32_t)pl.items;
     a.expect_combines = (int32_t)pl.combines;
     a.expect_partials = (int32_t)pl.partials;
+    a.total_tokens = (int32_t)sh.total_tokens;
+    a.max_blocks = geo->max_blocks_per_seq;
     return a;
 }
 
 gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
                        void* ws, hipStream_t stream) {
-    (void)geo;
-    return gc::launch_plan(plan_args(b, sh, pl, ws), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+    return gc::launch_plan(plan_args(geo, b, sh, pl, ws), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
 }
 
 // Pools of bf16 elements (fp8 false, scales 1) or of E4M3 codes with one scale each.
@@ -330,6 +336,7 @@ gc::AppendArgs append_args(const gc_geometry* geo, const gc_batch* batch, const 
     a.num_kv_heads = geo->num_kv_heads;
     a.num_blocks = geo->num_blocks;
     a.max_blocks = geo->max_blocks_per_seq;
+    a.total_pages = (int32_t)gc::append_pages_host(batch->prefix_lens_host, batch->new_lens_host, batch->batch);
     a.k_inv = 1.f / pk.k_scale;  // IEEE division: the same fl32(1 / scale) the definition uses
     a.v_inv = 1.f / pk.v_scale;
     return a;
@@ -365,7 +372,7 @@ gc_status prepare(const gc_geometry* geo, const gc_batch* batch, const gc_plan_o
     st = check_workspace(pl, workspace, workspace_bytes);
     if (st != GC_OK) return st;
     const gc::AppendArgs aa = append_args(geo, batch, sh, k_new, v_new, k_pool, v_pool, pk);
-    return gc::launch_prepare(aa, plan_args(batch, sh, pl, workspace), geo->head_dim, pk.fp8, stream) ==
+    return gc::launch_prepare(aa, plan_args(geo, batch, sh, pl, workspace), geo->head_dim, pk.fp8, stream) ==
                    hipSuccess
                ? GC_OK
                : GC_ERR_HIP;
@@ -537,6 +544,18 @@ gc_status gc_prefix_prefill_prepare_fp8(const gc_geometry* geo, const gc_batch* 
 }
 
 __attribute__((visibility("default")))
+gc_status gc_prefix_prefill_plan_status(const void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (workspace == nullptr) return GC_ERR_NULL_ARG;
+    if (workspace_bytes < sizeof(int32_t)) return GC_ERR_WORKSPACE;
+    static_assert(gc::kStatusOffset == 0, "the status word leads the workspace");
+    int32_t word = 0;
+    if (hipMemcpyAsync(&word, workspace, sizeof(word), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+        return GC_ERR_HIP;
+    return word == 0 ? GC_OK : GC_ERR_LENGTHS;
+}
+
+__attribute__((visibility("default")))
 gc_status gc_read_bandwidth_probe(const void* buf, size_t bytes, void* sink, hipStream_t stream) {
     if (buf == nullptr || sink == nullptr) return GC_ERR_NULL_ARG;
     if (bytes % 16 != 0) return GC_ERR_BAD_SHAPE;
@@ -567,6 +586,7 @@ const char* gc_status_string(gc_status s) {
         case GC_ERR_BLOCK_TABLE: return "GC_ERR_BLOCK_TABLE: block table too short for a request";
         case GC_ERR_WORKSPACE: return "GC_ERR_WORKSPACE: workspace missing or too small";
         case GC_ERR_HIP: return "GC_ERR_HIP: a HIP launch failed";
+        case GC_ERR_LENGTHS: return "GC_ERR_LENGTHS: the device length arrays disagree with the host's";
     }
     return "unknown gc_status";
 }

@@ -1,5 +1,5 @@
-// KV append kernel: one workgroup per 16 new tokens and KV head (the device code
-// is in append_body.h).
+// KV append kernel: one workgroup per pool page that receives new tokens and KV
+// head (the device code is in append_body.h).
 #include "append_body.h"
 
 namespace gc {
@@ -7,13 +7,15 @@ namespace {
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendArgs a) {
-    append_body<D, FP8>(a, (int)blockIdx.x, (int)blockIdx.y);
+    __shared__ AppendLds<D> lds;
+    append_body<D, FP8>(a, lds, (int)blockIdx.x, (int)blockIdx.y);
 }
 
 }  // namespace
 
 hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_t s) {
-    const dim3 grid((unsigned)ceil_div(a.total_tokens, kAppendTokens), (unsigned)a.num_kv_heads);
+    if (a.total_pages <= 0) return hipSuccess;
+    const dim3 grid((unsigned)a.total_pages, (unsigned)a.num_kv_heads);
     if (fp8) {
         if (head_dim == 128)
             append_kernel<128, true><<<grid, kAppendThreads, 0, s>>>(a);

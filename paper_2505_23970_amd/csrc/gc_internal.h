@@ -25,11 +25,10 @@ constexpr int kAttnThreads = kWaves * 64;
 constexpr int kWideWaves = 8;
 constexpr int kWideM = kRowsPerWave * kWideWaves;  // 256
 constexpr int kPlanThreads = 256;
-constexpr int kAppendTokens = 16;  // new tokens per append workgroup
 constexpr int kAppendThreads = 256;
 constexpr int kCostBuckets = 2048;  // counting-sort buckets of the work list (cost in tiles)
 constexpr int kCombineThreads = 256;  // threads per split-merge workgroup
-constexpr int kPlanLdsBatch = 2048;   // batches up to this size are planned from LDS copies
+constexpr int kPlanLdsBatch = 512;    // batches up to this size are planned from LDS copies
 constexpr int kProbeBlocks = 2048;    // read-probe grid
 constexpr int kProbeThreads = 256;
 constexpr int kMfmaProbeBlocks = 1024;   // matrix-core probe grid: four workgroups per CU
@@ -72,6 +71,15 @@ __host__ __device__ inline int split_begin(int s, int kt, int ns) {
     return (int)(((int64_t)s * kt) / ns);
 }
 
+// Pool pages that receive new tokens over the batch (the append grid), from the
+// host lengths: pages P_r / 16 .. (P_r + n_r - 1) / 16 of every request with n_r > 0.
+inline int64_t append_pages_host(const int32_t* prefix, const int32_t* n, int batch) {
+    int64_t u = 0;
+    for (int r = 0; r < batch; ++r)
+        if (n[r] > 0) u += ((int64_t)prefix[r] + n[r] + kPage - 1) / kPage - prefix[r] / kPage;
+    return u;
+}
+
 struct RequestCounts {
     int items;     // work items of this request (per KV head)
     int combines;  // query tiles that were split
@@ -93,6 +101,8 @@ __host__ __device__ inline RequestCounts request_counts(int prefix, int n, int t
 }
 
 // ---------------------------------------------------------------- workspace
+constexpr size_t kStatusOffset = 0;  // byte offset of the planner's status word in the workspace
+
 struct WorkspaceLayout {
     size_t items_off, combine_off, scratch_off, part_lse_off, part_o_off, status_off, total;
 };
@@ -102,7 +112,7 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 inline WorkspaceLayout workspace_layout(int batch, int64_t items, int64_t combines,
                                         int64_t partials, int num_kv_heads, int head_dim, int block_m) {
     WorkspaceLayout w{};
-    size_t off = 0;
+    size_t off = kStatusOffset;
     w.status_off = off;
     off = align_up(off + 256, 256);
     w.items_off = off;
@@ -130,6 +140,7 @@ struct AppendArgs {
     const int32_t* cu_new_lens;
     const int32_t* block_tables;
     int32_t batch, total_tokens, num_kv_heads, num_blocks, max_blocks;
+    int32_t total_pages;  // pool pages that receive new tokens (host count; the append grid)
     float k_inv, v_inv;  // 8-bit pools: fl32(1 / scale) of each pool
 };
 
@@ -140,9 +151,11 @@ struct PlanArgs {
     WorkItem* unsorted;       // [items]
     WorkItem* items;          // [items], sorted by cost, heaviest first
     CombineItem* combines;    // [combines]
-    int32_t* status;          // status[0] = 0 when the device counts matched the host's
+    int32_t* status;          // status[0] = 0 when the device lengths matched the host's
     int32_t batch, tq, chunk, block_n;
     int32_t expect_items, expect_combines, expect_partials;
+    int32_t total_tokens;     // the host's T (= cu_new_lens[batch] on the device)
+    int32_t max_blocks;       // row length of the block tables
 };
 
 struct AttnArgs {

@@ -5,7 +5,10 @@
 namespace gc {
 namespace {
 
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) { plan_body(a); }
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(const PlanArgs a) {
+    __shared__ PlanLds lds;
+    plan_body(a, lds);
+}
 
 }  // namespace
 

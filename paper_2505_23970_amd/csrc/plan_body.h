@@ -17,10 +17,13 @@
 // items start first (longest-processing-time scheduling). Order inside a cost
 // bucket and slot numbers may differ between runs; results do not depend on
 // them (every item writes its own outputs, merges run in chunk order).
-// If the device lengths do not reproduce the host's totals (the caller passed
-// different host and device arrays), every item is emitted empty and status[0]
-// is set to 1: the attention kernel then writes nothing, and nothing is
-// accessed out of bounds.
+// The device lengths are checked before anything is derived from them: cu[0]
+// must be 0, cu non-decreasing with cu[B] equal to the host's T, every prefix
+// length non-negative, every request's keys within the block-table row, and the
+// item, merge and partial counts equal to the host's. Otherwise (the caller
+// passed host and device arrays that disagree) every item is emitted empty and
+// status[0] is set to 1: the attention kernels then write nothing, and nothing
+// is accessed out of bounds. gc_prefix_prefill_plan_status reads the word.
 #pragma once
 #include "gc_internal.h"
 
@@ -88,27 +91,60 @@ __device__ __forceinline__ Tile tile_at(const PlanArgs& a, const Lens& l, int g)
     return t;
 }
 
+// LDS of the planner's workgroup (the caller provides it, so that a launch that
+// also runs the append can overlay the two).
+struct PlanLds {
+    int tmp[kPlanThreads];
+    int hist[kCostBuckets];
+    int part, comb, bad, badlen;
+    int cum[kPlanLdsBatch + 1], cu[kPlanLdsBatch + 1], pre[kPlanLdsBatch];
+};
+
 // The planner's workgroup (kPlanThreads threads).
-__device__ __forceinline__ void plan_body(const PlanArgs& a) {
-    __shared__ int s_tmp[kPlanThreads];
-    __shared__ int s_hist[kCostBuckets];
-    __shared__ int s_part, s_comb, s_bad;
-    __shared__ int s_cum[kPlanLdsBatch + 1], s_cu[kPlanLdsBatch + 1], s_pre[kPlanLdsBatch];
+__device__ __forceinline__ void plan_body(const PlanArgs& a, PlanLds& sm) {
+    int* const s_tmp = sm.tmp;
+    int* const s_hist = sm.hist;
+    int& s_part = sm.part;
+    int& s_comb = sm.comb;
+    int& s_bad = sm.bad;
+    int& s_badlen = sm.badlen;
+    int* const s_cum = sm.cum;
+    int* const s_cu = sm.cu;
+    int* const s_pre = sm.pre;
     const int tid = threadIdx.x;
     const bool small = a.batch <= kPlanLdsBatch;
     int* cum = small ? s_cum : a.scratch;  // [batch + 1]
+    if (tid == 0) s_badlen = 0;
     if (small) {
         for (int r = tid; r <= a.batch; r += kPlanThreads) {
             s_cu[r] = a.cu_new_lens[r];
             if (r < a.batch) s_pre[r] = a.prefix_lens[r];
         }
-        __syncthreads();
     }
+    __syncthreads();
     const Lens lens{cum, small ? s_cu : a.cu_new_lens, small ? s_pre : a.prefix_lens};
 
-    // 1. query tiles per request, scanned
+    // 0. the device lengths must describe the batch the host checked
     const int per = ceil_div(a.batch, kPlanThreads);
     const int r0 = min(a.batch, tid * per), r1 = min(a.batch, r0 + per);
+    {
+        bool bad = tid == 0 && (lens.cu[0] != 0 || lens.cu[a.batch] != a.total_tokens);
+        for (int r = r0; r < r1; ++r) {
+            const int64_t P = lens.prefix[r], c0 = lens.cu[r], n = (int64_t)lens.cu[r + 1] - c0;
+            bad |= P < 0 || n < 0 || P + n > (int64_t)INT32_MAX - kBlockN ||
+                   (n > 0 && ceil_div64(P + n, kPage) > a.max_blocks);
+        }
+        if (bad) s_badlen = 1;
+    }
+    __syncthreads();
+    if (s_badlen) {
+        for (int i = tid; i < a.expect_combines; i += kPlanThreads) a.combines[i] = CombineItem{0, 0, 0, 0};
+        for (int i = tid; i < a.expect_items; i += kPlanThreads) a.items[i] = WorkItem{-1, 0, 0, 0, -1, 0, 0, 0};
+        if (tid == 0) a.status[0] = 1;
+        return;
+    }
+
+    // 1. query tiles per request, scanned
     int mine = 0;
     for (int r = r0; r < r1; ++r)
         mine += ceil_div(lens.cu[r + 1] - lens.cu[r], a.tq);

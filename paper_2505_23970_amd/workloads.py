@@ -413,7 +413,7 @@ def document_trace(seed: int = SEED_BASE + 61, hours: float = 24.0, questions_pe
     """Document questions: `documents` documents with lognormal lengths (median
     4000 tokens, clipped to the 8k window); questions arrive as a Poisson process
     and pick a document with Zipf(alpha) popularity (the paper's alpha 0.4 and
-    0.7, §6.5); the cached entry is the document (context = document length),
+    0.7, §6.1); the cached entry is the document (context = document length),
     the question (median 20 tokens) is not reused."""
     rng = np.random.default_rng(seed)
     horizon = hours * 3600.0

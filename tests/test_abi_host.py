@@ -46,6 +46,12 @@ def test_mfma_probe_rejects_bad_arguments(lib):
     assert lib.gc_mfma_peak_probe(0, 0x2000, None) == 0       # nothing to run, nothing enqueued
 
 
+def test_plan_status_rejects_bad_arguments(lib):
+    """Checked before the copy of the status word (no HIP call)."""
+    assert lib.gc_prefix_prefill_plan_status(None, 256, None) == -1
+    assert lib.gc_prefix_prefill_plan_status(0x2000, 3, None) == -5
+
+
 def test_status_strings(lib):
     for code, name in gc.STATUS_NAMES.items():
         assert lib.gc_status_string(code).decode().startswith(name)

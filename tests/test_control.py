@@ -126,6 +126,28 @@ def test_carbon_model_matches_the_oracle():
         assert math.isclose(got, want, rel_tol=1e-12, abs_tol=1e-15)
 
 
+def test_carbon_model_hand_worked_examples():
+    """The product's carbon functions on the values worked by hand in
+    tests/golden/carbon_examples.json (independent of the oracle)."""
+    import json
+    from fractions import Fraction
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "carbon_examples.json")))
+    pp = g["platform"]
+    p = K.Platform(gpu_kg=pp["gpu_kg"], cpu_kg=pp["cpu_kg"], mem_kg=pp["mem_kg"],
+                   ssd_kg_per_tb=pp["ssd_kg_per_tb"], lifetime_years=pp["lifetime_years"],
+                   ssd_lifetime_years=pp["lifetime_years"])
+    bare = K.Platform(gpu_kg=0.0, cpu_kg=0.0, mem_kg=0.0, ssd_kg_per_tb=pp["ssd_kg_per_tb"],
+                      lifetime_years=pp["lifetime_years"], ssd_lifetime_years=pp["lifetime_years"])
+    value = lambda expr: float(sum(Fraction(t.strip()) for t in expr.split("+")))
+    for c in g["request_cases"]:
+        got = float(K.request_carbon_g(c["power_w"], c["ttft_s"], c["ci"], c["size_tb"],
+                                       p if c["with_others"] else bare))
+        assert math.isclose(got, value(c["expected"]), rel_tol=1e-12), c["name"]
+    for c in g["interval_cases"]:
+        got = float(K.interval_carbon_g(c["energy_kwh"], c["ci"], c["hours"], c["size_tb"], p))
+        assert math.isclose(got, value(c["expected"]), rel_tol=1e-12), c["name"]
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_ilp_solver_matches_bruteforce(seed):
     rng = np.random.default_rng(100 + seed)

@@ -145,6 +145,37 @@ def test_zero_intensity_leaves_only_embodied_carbon_and_no_cache_leaves_none_of_
     assert C.total_g(0.0, 124.0, 1.0, 0, 30, 5, []) == 0.0
 
 
+def golden_fraction(expr):
+    """A sum of fractions written in a golden file ("1/2 + 5/1314") as a float."""
+    from fractions import Fraction
+    return float(sum(Fraction(t.strip()) for t in expr.split("+")))
+
+
+def test_carbon_hand_worked_examples(C=C0):
+    """Per-request (Eq. ilp objective term) and per-interval (Eq. cache+other) carbon
+    against values worked by hand in tests/golden/carbon_examples.json: the W*s to
+    kWh conversion, the s to h conversion of the amortised terms, CI in g/kWh and
+    embodied kg in g are each visible in one of the cases."""
+    g = json.load(open(os.path.join(HERE, "golden", "carbon_examples.json")))
+    p = g["platform"]
+    others = [(p["gpu_kg"], p["lifetime_years"]), (p["cpu_kg"], p["lifetime_years"]),
+              (p["mem_kg"], p["lifetime_years"])]
+    for c in g["request_cases"]:
+        got = C.request_carbon_g(c["power_w"], c["ttft_s"], c["ci"], c["size_tb"], p["ssd_kg_per_tb"],
+                                 p["lifetime_years"], others if c["with_others"] else [])
+        assert math.isclose(got, golden_fraction(c["expected"]), rel_tol=1e-12), c["name"]
+    for c in g["interval_cases"]:
+        got = C.total_g(c["energy_kwh"], c["ci"], c["hours"], c["size_tb"], p["ssd_kg_per_tb"],
+                        p["lifetime_years"], others)
+        assert math.isclose(got, golden_fraction(c["expected"]), rel_tol=1e-12), c["name"]
+
+
+def test_operational_carbon_is_energy_times_intensity(C=C0):
+    """Eq. carbon-op at values that are not 0: 0.25 kWh at 400 g/kWh is 100 g."""
+    assert math.isclose(C.operational_g(0.25, 400.0), 100.0, rel_tol=1e-15)
+    assert math.isclose(C.operational_g(3.0, 56.0), 168.0, rel_tol=1e-15)
+
+
 # ----------------------------------------------------------------- cache-size ILP
 
 def knapsack_min_weight(w, v, V):
@@ -212,6 +243,13 @@ MUTANTS = {
     "ilp_ignores_tpot": ('if sum(ok_tpot[t][s] for t, s in enumerate(choice)) < need:',
                          'if False:'),
     "ilp_maximises": ('if c < best:', 'if best == math.inf or c > best:'),
+    "joules_to_kwh_off_by_1000": ('energy_kwh = power_w * ttft_s / 3.6e6', 'energy_kwh = power_w * ttft_s / 3.6e3'),
+    "ttft_taken_as_hours": ('hours = ttft_s / 3600.0', 'hours = ttft_s'),
+    "intensity_applied_in_kg": ('return energy_kwh * ci_g_per_kwh', 'return energy_kwh * ci_g_per_kwh / 1000.0'),
+    "embodied_left_in_kg": ('return hours / (lifetime_years * HOURS_PER_YEAR) * embodied_kg * 1000.0',
+                            'return hours / (lifetime_years * HOURS_PER_YEAR) * embodied_kg'),
+    "request_drops_other_embodied": ('return total_g(energy_kwh, ci, hours, size_tb, ssd_kg_per_tb, ssd_lifetime_years, others)',
+                                     'return total_g(energy_kwh, ci, hours, size_tb, ssd_kg_per_tb, ssd_lifetime_years, [])'),
 }
 
 PINS = [test_fifo_shows_beladys_anomaly, test_lru_textbook_fault_counts, test_lru_is_a_stack_algorithm,
@@ -221,7 +259,8 @@ PINS = [test_fifo_shows_beladys_anomaly, test_lru_textbook_fault_counts, test_lr
         test_amortised_share_over_the_whole_lifetime_is_the_whole_embodied_carbon,
         test_carbon_is_additive_over_time_and_capacity, test_ssd_table_entry_per_terabyte,
         test_zero_intensity_leaves_only_embodied_carbon_and_no_cache_leaves_none_of_its_own,
-        test_ilp_infeasible_when_no_choice_meets_the_slo]
+        test_ilp_infeasible_when_no_choice_meets_the_slo, test_carbon_hand_worked_examples,
+        test_operational_carbon_is_energy_times_intensity]
 
 
 def _run_pins(C):

@@ -47,19 +47,15 @@ def full_check(w, kv_split_tiles=None, rows=None, contract=False, tiling=None):
 
 # ----------------------------------------------------------------- the five workloads
 
-@pytest.mark.parametrize("k", [1, 2])
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_config_all_rows(k):
+    """Every output row of the five workloads (and the whole pool after the append)
+    against the fp64 oracle, in the tiling and split the automatic plan picks, which
+    is what the benchmark times."""
     w = W.make_config(k)
     info, _, _ = full_check(w, contract=True)
-    say(f"config {k}: {info}")
-
-
-@pytest.mark.parametrize("k", [3, 4, 5])
-def test_config_sampled_rows(k):
-    w = W.make_config(k)
-    rows = H.sample_rows(w, seed=k)
-    info, _, _ = full_check(w, rows=rows, contract=True)
-    say(f"config {k}: {len(rows)} rows {info}")
+    say(f"config {k}: {w.total_new * w.num_q_heads} rows {info}")
 
 
 def test_decode_workload_sampled():
@@ -133,10 +129,11 @@ def test_needle_in_prefix_and_in_new_tokens(split):
 
 @pytest.mark.parametrize("split", [None, 1])
 def test_values_one_normalises(split):
-    """V = 1: the output is the sum of the weights. The probabilities enter the PV
-    product rounded to bf16 (relative error <= 2^-8 each) while the normaliser sums
-    them unrounded, so the result is 1 within 2^-8 and then rounds to 1.0 or to
-    the bf16 value just below it; nearly every row lands exactly on 1.0."""
+    """V = 1: the output is the sum of the weights over the normaliser. The
+    probabilities enter the PV product rounded to bf16 and the normaliser sums the
+    same bf16-rounded weights, so the quotient is 1 up to fp32 summation order
+    (chunk merges and the two partial sums of a row) and rounds to 1.0 in bf16;
+    the bound allows 2^-8 and nearly every row lands exactly on 1.0."""
     w = W.set_values_one(W.build(seed=102, values="unit", name="v_one", **SUITE_SHAPE))
     _, _, out = full_check(w, kv_split_tiles=split)
     got = H.from_dev_f32(out)
@@ -159,9 +156,10 @@ def test_position_code_window(split):
 
 @pytest.mark.parametrize("split", [None, 1])
 def test_score_jump_beyond_offset_slack(split):
-    """A key whose score exceeds the earlier ones by ~130 in log2 units (more than the
-    kernel's 2^64 offset slack): the exponent offset set by the first tile is too small
-    and the work item must be redone with the larger one (fp32 would overflow otherwise)."""
+    """A key whose score exceeds the earlier ones by ~130 in log2 units: the kernels
+    keep a running exponent offset and rescale the accumulators only when a tile's
+    maximum exceeds it by more than 2^8, so this jump must trigger a rescale (without
+    one the weights exp2(130) would overflow fp32 and the output would be NaN or Inf)."""
     w = W.build([300, 70], [40, 9], 8, 1, 128, seed=104, name="score_jump")
     w.q[:, :, 0] = W.f32_to_bf16_bits(np.float32(8.0))
     w.k_prefix[250, :, 0] = W.f32_to_bf16_bits(np.float32(128.0))  # request 0, position 250
@@ -306,6 +304,43 @@ def test_pool_beyond_4_gib(kv, tiling):
         assert torch.equal(big[shift:].view(torch.uint8), small.view(torch.uint8))
     del pools
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("split", [None, 1])
+@pytest.mark.parametrize("case", ["agree", "device_total_longer", "negative_prefix", "table_too_short"])
+def test_plan_status_reports_disagreeing_lengths(case, split):
+    """The planner checks the device lengths against the host's: when they disagree the
+    plan status is GC_ERR_LENGTHS and a run on that plan leaves out and lse untouched
+    (NaN sentinels); when they agree the status is GC_OK and the output is the oracle's."""
+    import torch
+    import paper_2505_23970_amd as gc
+    w = W.build([300, 17, 96], [37, 5, 64], 16, 2, 128, seed=340, values="unit", name="plan_status")
+    say(f"case plan status: {case} split={split}")
+    run = H.DeviceRun(w)
+    run.append()
+    batch = gc.PagedBatch(w.prefix_lens, w.new_lens, w.block_tables)
+    if case == "device_total_longer":      # request 1 has 3 more new tokens on the device
+        batch.cu_new_lens_dev[2:] += 3
+    elif case == "negative_prefix":
+        batch.prefix_lens_dev[1] = -40
+    elif case == "table_too_short":        # request 0's keys run past its table row
+        batch.prefix_lens_dev[0] = 16 * w.block_tables.shape[1]
+    T, Hq, D = w.q.shape
+    ws = gc.alloc_workspace(Hq, run.k_pool, run.v_pool, batch, kv_split_tiles=split)
+    gc.plan(Hq, run.k_pool, run.v_pool, batch, ws, kv_split_tiles=split)
+    status = gc.plan_status(ws)
+    out = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+    gc.run(run.q, run.k_pool, run.v_pool, batch, w.scale, ws, out=out, lse=lse, kv_split_tiles=split)
+    torch.cuda.synchronize()
+    if case == "agree":
+        assert status == gc.GC_OK
+        kp, vp = H.oracle_pools(w)
+        ref, ref_lse = H.oracle_rows(w, kp, vp)
+        H.compare_attention(w, out, lse, ref, ref_lse)
+    else:
+        assert status == gc.GC_ERR_LENGTHS
+        assert torch.isnan(out.float()).all().item() and torch.isnan(lse).all().item()
 
 
 def test_plan_once_run_twice():
@@ -462,8 +497,13 @@ def test_restore_prefix_from_host_tier(source):
         ks, vs = ks.cuda(), vs.cuda()
     gc.kv_restore(ks, vs, kp, vp, run.batch)
     torch.cuda.synchronize()
-    assert np.array_equal(H.from_dev_bits(kp), w.k_pool)
-    assert np.array_equal(H.from_dev_bits(vp), w.v_pool)
+    # expected image: the oracle's append of the prefixes (prefix lengths 0, new
+    # lengths P_r) into the same all-NaN pools
+    zero = np.zeros_like(w.prefix_lens)
+    kref, vref = H.oracle.kv_append(zero, w.prefix_lens, w.block_tables, w.num_blocks,
+                                    w.k_prefix, w.v_prefix, nan, np.full_like(w.v_pool, W.BF16_NAN))
+    assert np.array_equal(H.from_dev_bits(kp), kref)
+    assert np.array_equal(H.from_dev_bits(vp), vref)
 
 
 def test_restore_refuses_pageable_host_memory():
@@ -519,14 +559,18 @@ def fp8_check(w, ks, vs, kv_split_tiles=None, tiling=None, rows=None, contract=T
     return H.compare_attention(w, out, lse, ref_out, ref_lse, rows=rows, contract=contract, vmax=vmax)
 
 
+@pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("split", [None, 2])
 @pytest.mark.parametrize("tiling", ["prefill", "wide", "small"])
-def test_fp8_pools_every_tiling(tiling, split):
+def test_fp8_pools_every_tiling(tiling, split, D):
+    """Every tiling over 8-bit pools, with and without key splits, at both head
+    dimensions (each (tiling, D) pair is its own kernel instance)."""
     import paper_2505_23970_amd as gc
     t = {"prefill": gc.TILES_PREFILL, "wide": gc.TILES_WIDE, "small": gc.TILES_SMALL}[tiling]
-    w = W.build(seed=110, name=f"fp8_{tiling}", **SUITE_SHAPE)
+    shape = dict(SUITE_SHAPE, head_dim=D)
+    w = W.build(seed=110 + D, name=f"fp8_{tiling}_d{D}", **shape)
     info = fp8_check(w, 0.0113, 0.0271, kv_split_tiles=split, tiling=t)
-    say(f"8-bit {tiling} split {split}: {info}")
+    say(f"8-bit {tiling} D={D} split {split}: {info}")
 
 
 @pytest.mark.parametrize("D", [64, 128])
@@ -542,6 +586,14 @@ def test_fp8_config2_all_rows():
     w = W.make_config(2)
     info = fp8_check(w, 2.0 ** -6, 0.0213)
     say(f"8-bit config 2: {info}")
+
+
+@pytest.mark.timeout(600)
+def test_fp8_long_reuse_sampled():
+    """The 32k-prefix workload over 8-bit pools (automatic plan: key splits), sampled rows."""
+    w = W.make_config(4)
+    info = fp8_check(w, 2.0 ** -6, 0.0213, rows=H.sample_rows(w, seed=44))
+    say(f"8-bit config 4: {info}")
 
 
 def test_fp8_decode_workload_sampled():
