@@ -196,6 +196,27 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       hipStream_t stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): gc_prefix_prefill_attention
+ * without a workspace argument. The plan and the split-KV partials go to a
+ * static device array of GC_NOALLOC_SCRATCH_BYTES bytes that the library holds
+ * on every GPU it runs on until the process ends; this call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine). Arguments, layouts,
+ * results and errors are those of gc_prefix_prefill_attention, plus
+ * GC_ERR_WORKSPACE (nothing enqueued) when the batch's workspace
+ * (gc_prefix_prefill_workspace_size) exceeds GC_NOALLOC_SCRATCH_BYTES. Every
+ * word the kernels read is written by the same call's plan first, so nothing
+ * needs clearing between calls. All calls on one GPU share its array: calls
+ * whose work overlaps on one GPU (two streams, or two host threads) race and
+ * must be serialised by the caller; calls in one stream are ordered.
+ */
+#define GC_NOALLOC_SCRATCH_BYTES (64u << 20)
+gc_status gc_prefix_prefill_attention_noalloc(const gc_geometry* geo, const gc_batch* batch,
+                                              const gc_plan_options* opts,
+                                              const void* q, const void* k_pool, const void* v_pool,
+                                              float scale, void* out, float* lse, hipStream_t stream);
+
+/*
  * gc_kv_append followed by gc_prefix_prefill_plan, as one launch: the two are
  * independent (the plan reads only the lengths), so one launch overlaps them
  * and saves a kernel boundary in a step that appends and attends once per

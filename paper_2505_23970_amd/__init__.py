@@ -27,7 +27,7 @@ EXPORTED = ("gc_kv_append", "gc_prefix_prefill_workspace_size", "gc_prefix_prefi
             "gc_prefix_prefill_run", "gc_prefix_prefill_attention", "gc_kv_append_fp8",
             "gc_prefix_prefill_run_fp8", "gc_prefix_prefill_attention_fp8", "gc_prefix_prefill_prepare",
             "gc_prefix_prefill_prepare_fp8", "gc_prefix_prefill_run_with_append",
-            "gc_prefix_prefill_plan_status", "gc_read_bandwidth_probe",
+            "gc_prefix_prefill_plan_status", "gc_prefix_prefill_attention_noalloc", "gc_read_bandwidth_probe",
             "gc_mfma_peak_probe", "gc_status_string")
 READ_PROBE_SINK_WORDS = 2048 * 256
 MFMA_PROBE_SINK_FLOATS = 1024 * 256
@@ -107,6 +107,8 @@ def load_library(path: str | None = None):
     lib.gc_prefix_prefill_run_with_append.restype = i32
     lib.gc_prefix_prefill_run_with_append.argtypes = [G, Bp, O, vp, vp, vp, vp, vp, f32, vp, vp, vp,
                                                       ctypes.c_size_t, vp]
+    lib.gc_prefix_prefill_attention_noalloc.restype = i32
+    lib.gc_prefix_prefill_attention_noalloc.argtypes = [G, Bp, O, vp, vp, vp, ctypes.c_float, vp, vp, vp]
     lib.gc_prefix_prefill_plan_status.restype = i32
     lib.gc_prefix_prefill_plan_status.argtypes = [vp, ctypes.c_size_t, vp]
     lib.gc_read_bandwidth_probe.restype = i32
@@ -309,6 +311,25 @@ def plan(num_q_heads, k_pool, v_pool, batch: PagedBatch, workspace, kv_split_til
                                     _opts(kv_split_tiles, tiling), workspace.data_ptr(),
                                     workspace.numel(), _stream_handle(stream))
     _check("gc_prefix_prefill_plan", st, lib)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def prefix_prefill_attention_noalloc(q, k_pool, v_pool, batch: PagedBatch, scale, out=None, lse=None,
+                                     kv_split_tiles=None, stream=None, tiling=None):
+    """gc_prefix_prefill_attention_noalloc: plan and attention with the library's own
+    static device scratch instead of a caller workspace (for callers that cannot
+    allocate). Calls that overlap on one GPU race on that scratch."""
+    lib = load_library()
+    geo, out = _attn_args(q, k_pool, v_pool, batch, out, lse, None)
+    st = lib.gc_prefix_prefill_attention_noalloc(ctypes.byref(geo), ctypes.byref(batch.desc()),
+                                                 _opts(kv_split_tiles, tiling), q.data_ptr(), k_pool.data_ptr(),
+                                                 v_pool.data_ptr(), float(scale), out.data_ptr(),
+                                                 lse.data_ptr() if lse is not None else None,
+                                                 _stream_handle(stream))
+    _check("gc_prefix_prefill_attention_noalloc", st, lib)
+    return out
 
 
 def plan_status(workspace, stream=None) -> int:

@@ -401,6 +401,43 @@ gc_status run(const gc_geometry* geo, const gc_batch* batch, const gc_plan_optio
     return enqueue_run(geo, batch, sh, pl, q, k_pool, v_pool, scale, out, lse, workspace, stream, pk);
 }
 
+// ---------------------------------------------------------------- no-allocation variant
+// Workspace of gc_prefix_prefill_attention_noalloc: one file-scope device array per
+// GPU the library runs on (held until the process ends). Host code never passes the
+// array's name to a kernel or a copy: in host code it is a host-side stand-in, not
+// a device address. The device address comes from hipGetSymbolAddress, taken once
+// per device with that device current, and is kept per device.
+static __device__ __align__(256) unsigned char scratch[GC_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+struct DeviceScratch {
+    std::once_flag once;
+    void* ptr = nullptr;
+    hipError_t err = hipSuccess;
+};
+DeviceScratch g_scratch[kMaxDevices];
+
+// Device address of the current device's scratch array (nullptr and a status on failure).
+void* scratch_address(gc_status* st) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+        *st = GC_ERR_HIP;
+        return nullptr;
+    }
+    if (dev >= kMaxDevices) {
+        *st = GC_ERR_UNSUPPORTED;
+        return nullptr;
+    }
+    DeviceScratch& d = g_scratch[dev];
+    std::call_once(d.once, [&d]() { d.err = hipGetSymbolAddress(&d.ptr, HIP_SYMBOL(scratch)); });
+    if (d.err != hipSuccess || d.ptr == nullptr) {
+        *st = GC_ERR_HIP;
+        return nullptr;
+    }
+    *st = GC_OK;
+    return d.ptr;
+}
+
 // Append and run from a plan already in the workspace. Prefill tiles: one launch
 // (the work items read the new keys from k_new / v_new and write their own tokens'
 // K/V into the pools). Small tiles read every key from the pool, so there the append
@@ -492,6 +529,25 @@ gc_status gc_prefix_prefill_attention(const gc_geometry* geo, const gc_batch* ba
                                       size_t workspace_bytes, hipStream_t stream) {
     return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, workspace, workspace_bytes,
                stream, true, PoolKind{});
+}
+
+__attribute__((visibility("default")))
+gc_status gc_prefix_prefill_attention_noalloc(const gc_geometry* geo, const gc_batch* batch,
+                                              const gc_plan_options* opts, const void* q,
+                                              const void* k_pool, const void* v_pool, float scale,
+                                              void* out, float* lse, hipStream_t stream) {
+    // every host check first (workspace size included), then the device address
+    Shape sh;
+    Plan pl;
+    gc_status st = plan_checked(geo, batch, opts, &sh, &pl);
+    if (st != GC_OK || sh.total_tokens == 0) return st;
+    st = check_run_args(q, k_pool, v_pool, scale, out);
+    if (st != GC_OK) return st;
+    if (pl.layout.total > (size_t)GC_NOALLOC_SCRATCH_BYTES) return GC_ERR_WORKSPACE;
+    void* ws = scratch_address(&st);
+    if (ws == nullptr) return st;
+    return run(geo, batch, opts, q, k_pool, v_pool, scale, out, lse, ws, GC_NOALLOC_SCRATCH_BYTES, stream,
+               true, PoolKind{});
 }
 
 __attribute__((visibility("default")))
