@@ -201,6 +201,19 @@ def test_edge_cases(name, P, n, Hq, Hkv, D):
         full_check(w, kv_split_tiles=1, tiling=gc.TILES_SMALL)
 
 
+@pytest.mark.parametrize("split", [None, 1, 2, 3, 7])
+def test_below_ridge_on_prefill_tiles(split):
+    """Batches below the ridge (few new tokens, long prefixes) on 128-row tiles: work
+    items of 1 to 60 key tiles, page tails, a miss and a one-token request, with and
+    without key splits, at both head dimensions."""
+    import paper_2505_23970_amd as gc
+    w = W.build([0, 50, 130, 190, 3000, 1, 700], [9, 3, 1, 16, 12, 5, 2], 16, 2, 128, seed=270,
+                values="unit", name="below_ridge")
+    full_check(w, kv_split_tiles=split, tiling=gc.TILES_PREFILL)
+    w64 = W.build([64, 1234, 5], [16, 4, 40], 8, 1, 64, seed=271, values="peaked", name="below_ridge_d64")
+    full_check(w64, kv_split_tiles=split, tiling=gc.TILES_PREFILL)
+
+
 def test_batch_beyond_lds_plan_limit():
     """More requests than the planner keeps in LDS (2048): the work list is built
     from the global length arrays instead."""
