@@ -307,11 +307,16 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     };
 
     f32x16 o[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
-    float m_run = -INFINITY;  // max of score * scale * log2(e) used as the exponent offset
-    float l_run = 0.f;        // this lane's half of the row sum of the bf16 weights,
-    float l_run1 = 0.f;       // accumulated in two independent sums
+    float m_run;   // exponent offset (score * scale * log2(e) units)
+    float l_run;   // this lane's half of the row sum of the bf16 weights,
+    float l_run1;  // accumulated in two independent sums
+    // Exponent offset: a row takes the maximum of its first tile with a visible key and
+    // keeps it; the weights of later tiles are exp2 of up to ~100 and fp32 holds their
+    // products and sums. If some row's sum leaves that range (a score jump of more than
+    // ~100 in log2 units), the work item is run again with the exact running maximum of
+    // every tile (rescaled lazily, when it grows by more than 2^8). The final
+    // normalisation uses the same offset, so the result does not depend on it.
+    bool exact = false;
     const float c = a.scale_log2;
     // key row fed to the QK^T product by this lane: bits 2 and 3 of lr swapped
     const int prow = (lr & 0x13) | ((lr & 4) << 1) | ((lr & 8) >> 1);
@@ -364,6 +369,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
         }
         // row maximum: NaN-propagating maxima need no operand canonicalisation and
         // fold three operands per instruction
+        if (exact || __any(m_run == -INFINITY)) {
         float mx = s[0][0], mx1 = s[1][0];  // two independent chains
 #pragma unroll
         for (int e = 1; e < 16; ++e) {
@@ -386,6 +392,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
             l_run1 *= alpha;
 #pragma unroll
             for (int db = 0; db < DB; ++db) o[db] *= alpha;
+        }
         }
         const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
         __builtin_amdgcn_sched_barrier(0);
@@ -601,6 +608,13 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
             for (int p = 0; p < 4; ++p) bl_cur[p] = bl_next[p];
     };
 
+    for (;;) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) o[db] = f32x16{};
+    m_run = -INFINITY;
+    l_run = 0.f;
+    l_run1 = 0.f;
+    kt = it.kt_begin;
     fetch_ids(kt, ids);
     if constexpr (FP8) {
         load8(kt, ids);
@@ -623,6 +637,9 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
         if (++kt >= it.kt_end) break;
         step(k_lds1, v_lds1, k_lds0, v_lds0);
         if (++kt >= it.kt_end) break;
+    }
+    if (exact || !__syncthreads_or(!(l_run + l_run1 <= 0x1p100f))) break;
+    exact = true;
     }
 
     l_run += l_run1;

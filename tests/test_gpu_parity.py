@@ -156,10 +156,11 @@ def test_position_code_window(split):
 
 @pytest.mark.parametrize("split", [None, 1])
 def test_score_jump_beyond_offset_slack(split):
-    """A key whose score exceeds the earlier ones by ~130 in log2 units: the kernels
-    keep a running exponent offset and rescale the accumulators only when a tile's
-    maximum exceeds it by more than 2^8, so this jump must trigger a rescale (without
-    one the weights exp2(130) would overflow fp32 and the output would be NaN or Inf)."""
+    """A key whose score exceeds the earlier ones by ~130 in log2 units. The prefill
+    tiles keep the exponent offset of a row's first tile and run the work item again
+    with exact running maxima when a row's weight sum overflows; the small tiles
+    rescale when a tile's maximum exceeds the offset by more than 2^8. Either way this
+    jump must be absorbed (weights of exp2(130) would overflow fp32: NaN or Inf)."""
     w = W.build([300, 70], [40, 9], 8, 1, 128, seed=104, name="score_jump")
     w.q[:, :, 0] = W.f32_to_bf16_bits(np.float32(8.0))
     w.k_prefix[250, :, 0] = W.f32_to_bf16_bits(np.float32(128.0))  # request 0, position 250
