@@ -610,6 +610,28 @@ def test_fp8_long_reuse_sampled():
     say(f"8-bit config 4: {info}")
 
 
+@pytest.mark.parametrize("split", [None, 1, 2, 3, 4, 5, 7])
+def test_fp8_below_ridge_on_prefill_tiles(split):
+    """8-bit pools, batches below the ridge on 128-row tiles: work items of 1 to 60 key
+    tiles, page tails, a miss and a one-token request, with and without key splits, at
+    both head dimensions."""
+    import paper_2505_23970_amd as gc
+    w = W.build([0, 50, 130, 190, 3000, 1, 700], [9, 3, 1, 16, 12, 5, 2], 16, 2, 128, seed=272,
+                name="fp8_below_ridge")
+    info = fp8_check(w, 0.02, 0.015, kv_split_tiles=split, tiling=gc.TILES_PREFILL)
+    say(f"8-bit below ridge split {split}: {info}")
+    w64 = W.build([64, 1234, 5], [16, 4, 40], 8, 1, 64, seed=273, name="fp8_below_ridge_d64")
+    fp8_check(w64, 0.0113, 0.0271, kv_split_tiles=split, tiling=gc.TILES_PREFILL)
+
+
+def test_fp8_short_suffix_variant_sampled():
+    """The 32k-prefix workload with 16 new tokens per request over 8-bit pools (automatic
+    key splits), sampled rows."""
+    w = W.short_suffix_variant()
+    info = fp8_check(w, 2.0 ** -6, 0.0213, rows=H.sample_rows(w, seed=41))
+    say(f"8-bit long reuse, 16 new tokens: {info}")
+
+
 def test_fp8_decode_workload_sampled():
     w = W.decode_variant()
     info = fp8_check(w, 2.0 ** -6, 0.0213, rows=H.sample_rows(w, seed=51))
