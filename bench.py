@@ -385,7 +385,6 @@ def main():
         restore_benchmark(w, max(args.steps // 10, 5), min(args.warmup, 5))
         return
     fp8 = args.kv == "fp8"
-    ramp_clocks()
     m = measure(w, args.steps, args.warmup, fp8, args.kv_split_tiles)
     rec = {
         "metric": METRIC,
@@ -419,10 +418,11 @@ def main():
 
 
 def ramp_clocks(seconds=0.25):
-    """Untimed: run the matrix-core probe for a fraction of a second first. An idle GPU
-    raises its clocks over the first ~40 ms of sustained work, which would otherwise
-    fall into the first warm-up steps (all of them, with few warm-up steps of a short
-    workload); a serving loop runs in the steady state."""
+    """Untimed: run the matrix-core probe for a fraction of a second before a workload's
+    warm-up. An idle GPU (it idles while the host draws and uploads a workload) raises its
+    clocks over the first ~40 ms of sustained work, which would otherwise fall into the
+    first warm-up steps (all of them, with few warm-up steps of a short workload); a
+    serving loop runs in the steady state."""
     import torch
     import paper_2505_23970_amd as gc
     sink = gc.mfma_peak_probe(1)
@@ -459,6 +459,9 @@ def measure(w, steps, warmup, fp8, kv_split_tiles):
     out = torch.empty_like(q)
     ws = gc.alloc_workspace(Hq, k_pool, v_pool, batch, kv_split_tiles)
     torch.cuda.synchronize()
+    # the GPU idled while this workload was drawn and uploaded: bring its clocks back up
+    # before the warm-up steps
+    ramp_clocks()
 
     def step(ev=None):
         # append and plan in one launch, then the attention
