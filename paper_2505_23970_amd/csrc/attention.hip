@@ -130,10 +130,11 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     const WorkItem it = a.items[blockIdx.x / (unsigned)a.num_kv_heads];
     if (it.r < 0 || it.kt_begin >= it.kt_end) return;
 
+    // (the planner repeats the request's lengths in the item: one load for all of them)
     const int r = it.r;
-    const int P = a.prefix_lens[r];
-    const int cu = a.cu_new_lens[r];
-    const int n = a.cu_new_lens[r + 1] - cu;
+    const int P = it.P;
+    const int cu = it.cu;
+    const int n = it.n;
     const int L = P + n;
     const int ntok = min(a.tq, n - it.q0);
 
@@ -648,18 +649,41 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     const float lse_v = l_tot > 0.f ? (m_run + log2f(l_tot)) * kLn2 : -INFINITY;
     // o[db][4j + i] is element d = 32db + 8j + 4hh + i of this lane's row
     if (it.part < 0) {
-        if (row_ok) {
-            uint16_t* op = a.out + qrow * D;
+        // Output rows go through LDS so that every store writes whole rows: a lane's own
+        // values cover 16 bytes of each of 32 rows, 256 bytes apart. The tiles are no
+        // longer read (the last barrier above), so each wavefront takes 8 KiB (4 KiB for
+        // d = 64) of the tile buffers: its 32 rows, 16-byte chunks XOR-swizzled by row.
+        // Each store then covers 256 (128) contiguous bytes of 4 (8) rows, and the rows
+        // of one token's query heads are adjacent in the output.
+        constexpr int RB = 2 * D;                       // bytes per row
+        constexpr int CH = RB / 16;                     // 16-byte chunks per row
+        constexpr int kStage = kRowsPerWave * RB;       // bytes per wavefront
+        constexpr int kPerBuf = kTileBytes / kStage;    // wavefronts per tile buffer
+        static_assert(kPerBuf * 4 >= WAVES && kPerBuf * kStage == kTileBytes, "stage layout");
+        const int sb = wave / kPerBuf;
+        unsigned char* stage = (sb == 0 ? k_lds0 : sb == 1 ? v_lds0 : sb == 2 ? k_lds1 : v_lds1) +
+                               (wave % kPerBuf) * kStage;
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    u32x2 w;
-                    w[0] = pack_bf16x2(o[db][4 * j] * inv, o[db][4 * j + 1] * inv);
-                    w[1] = pack_bf16x2(o[db][4 * j + 2] * inv, o[db][4 * j + 3] * inv);
-                    *reinterpret_cast<u32x2*>(op + 32 * db + 8 * j + 4 * hh) = w;
-                }
-            if (a.lse != nullptr && hh == 0) a.lse[qrow] = lse_v;
+            for (int j = 0; j < 4; ++j) {
+                u32x2 w;
+                w[0] = pack_bf16x2(o[db][4 * j] * inv, o[db][4 * j + 1] * inv);
+                w[1] = pack_bf16x2(o[db][4 * j + 2] * inv, o[db][4 * j + 3] * inv);
+                *reinterpret_cast<u32x2*>(stage + lr * RB + ((4 * db + j) ^ (lr & (CH - 1))) * 16 + 8 * hh) = w;
+            }
+        if (row_ok && a.lse != nullptr && hh == 0) a.lse[qrow] = lse_v;
+        constexpr int kRowsPerStore = 64 / CH;
+#pragma unroll
+        for (int i = 0; i < kRowsPerWave / kRowsPerStore; ++i) {
+            const int rr = i * kRowsPerStore + lane / CH, ch = lane % CH;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(stage + rr * RB + (ch ^ (rr & (CH - 1))) * 16);
+            const int mr = wave * kRowsPerWave + rr;  // the stored row's token and head
+            const int tr = mr / a.group;
+            if (tr < ntok) {
+                const int64_t qr = (int64_t)(cu + it.q0 + tr) * a.num_q_heads + kvh * a.group + (mr - tr * a.group);
+                *reinterpret_cast<u32x4*>(a.out + qr * D + ch * 8) = v;
+            }
         }
     } else {
         const int64_t prow_g = ((int64_t)it.part * a.num_kv_heads + kvh) * kBlockRows + m;

@@ -38,8 +38,11 @@ constexpr int kMfmaProbePerChain = 4;    // products per accumulator per iterati
 // One attention work item: query tile [q0, q0 + tq) of request r against key
 // tiles [kt_begin, kt_end). part >= 0 marks a split item whose normalised
 // partial output goes to partial slot `part`; -1 writes the output directly.
+// r < 0 marks an empty item. P, cu and n repeat the request's prefix length,
+// first new row and new-token count, so that one load gives all of an item's
+// lengths.
 struct WorkItem {
-    int32_t r, q0, kt_begin, kt_end, part, pad0, pad1, pad2;
+    int32_t r, q0, kt_begin, kt_end, part, P, cu, n;
 };
 
 // One query tile whose keys were split: partial slots [part_base, part_base + ns).

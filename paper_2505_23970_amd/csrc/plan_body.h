@@ -215,7 +215,8 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, PlanLds& sm) {
             const int b0 = split_begin(s, t.kt, t.ns), b1 = split_begin(s + 1, t.kt, t.ns);
             const int pos = b1 - b0 == lo ? pos_lo++ : pos_hi++;
             a.items[pos] = part0 == -2 ? WorkItem{-1, 0, 0, 0, -1, 0, 0, 0}
-                                       : WorkItem{t.r, t.q0, b0, b1, part0 < 0 ? -1 : part0 + s, 0, 0, 0};
+                                       : WorkItem{t.r, t.q0, b0, b1, part0 < 0 ? -1 : part0 + s, lens.prefix[t.r],
+                                                  lens.cu[t.r], lens.cu[t.r + 1] - lens.cu[t.r]};
         }
     }
     __syncthreads();
