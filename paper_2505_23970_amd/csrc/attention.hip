@@ -85,6 +85,16 @@ __device__ __forceinline__ void wait_vmem() {
     asm volatile("" ::: "memory");  // no LDS access moves above the wait
 }
 
+// The lanes of one wavefront exchange data through LDS: a release and an acquire at
+// wavefront scope between the writes and the reads, so the compiler neither reuses
+// values a lane loaded earlier nor moves the reads across the writes of other lanes
+// (the hardware runs one wavefront's LDS operations in order).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Sixteen E4M3 codes (four words) as sixteen bf16 values (eight words).
 __device__ __forceinline__ void widen_e4m3x16(const u32x4 c, u32x4& lo, u32x4& hi) {
     uint32_t w[8];
@@ -673,6 +683,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
                 *reinterpret_cast<u32x2*>(stage + lr * RB + ((4 * db + j) ^ (lr & (CH - 1))) * 16 + 8 * hh) = w;
             }
         if (row_ok && a.lse != nullptr && hh == 0) a.lse[qrow] = lse_v;
+        wave_lds_sync();
         constexpr int kRowsPerStore = 64 / CH;
 #pragma unroll
         for (int i = 0; i < kRowsPerWave / kRowsPerStore; ++i) {
@@ -686,17 +697,44 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
             }
         }
     } else {
-        const int64_t prow_g = ((int64_t)it.part * a.num_kv_heads + kvh) * kBlockRows + m;
-        float* po = a.part_o + prow_g * D;
+        // Partial rows (fp32) of a split item, through the same stage: the wavefront's 32
+        // rows are contiguous in the partial buffer, so each store covers whole rows; rows
+        // larger than the stage go in rounds of kRows.
+        constexpr int RB = 4 * D;                             // bytes per fp32 row
+        constexpr int CH = RB / 16;                           // 16-byte chunks per row
+        constexpr int kStage = 4 * kTileBytes / WAVES;        // stage bytes per wavefront
+        constexpr int kRows = kStage / RB < kRowsPerWave ? kStage / RB : kRowsPerWave;
+        static_assert(kRows >= 2 && kRowsPerWave % kRows == 0 && (kRows * CH) % 64 == 0, "partial stage");
+        constexpr int kPerBuf = kTileBytes / kStage;
+        const int sb = wave / kPerBuf;
+        unsigned char* stage = (sb == 0 ? k_lds0 : sb == 1 ? v_lds0 : sb == 2 ? k_lds1 : v_lds1) +
+                               (wave % kPerBuf) * kStage;
+        const int64_t prow0 = ((int64_t)it.part * a.num_kv_heads + kvh) * kBlockRows + wave * kRowsPerWave;
+        constexpr int kSw = CH < 16 ? CH : 16;                // chunk swizzle span
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+        for (int r0 = 0; r0 < kRowsPerWave; r0 += kRows) {
+            if (lr >= r0 && lr < r0 + kRows) {
+                const int sr = lr - r0;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                f32x4 w = {o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
-                           o[db][4 * j + 3] * inv};
-                *reinterpret_cast<f32x4*>(po + 32 * db + 8 * j + 4 * hh) = w;
+                for (int db = 0; db < DB; ++db)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        f32x4 w = {o[db][4 * j] * inv, o[db][4 * j + 1] * inv, o[db][4 * j + 2] * inv,
+                                   o[db][4 * j + 3] * inv};
+                        const int ch = (8 * db + 2 * j + hh) ^ (sr & (kSw - 1));
+                        *reinterpret_cast<f32x4*>(stage + sr * RB + ch * 16) = w;
+                    }
             }
-        if (hh == 0) a.part_lse[prow_g] = lse_v;
+            wave_lds_sync();
+#pragma unroll
+            for (int i = 0; i < kRows * CH / 64; ++i) {
+                const int c = i * 64 + lane, sr = c / CH, ch = c % CH;
+                const f32x4 v = *reinterpret_cast<const f32x4*>(stage + sr * RB + (ch ^ (sr & (kSw - 1))) * 16);
+                *reinterpret_cast<f32x4*>(a.part_o + (prow0 + r0 + sr) * D + ch * 4) = v;
+            }
+            wave_lds_sync();  // the next round overwrites the stage
+        }
+        if (hh == 0) a.part_lse[prow0 + lr] = lse_v;
     }
 }
 
