@@ -26,6 +26,7 @@ struct Shape {
 struct Plan {
     int chunk = 0;  // key tiles per chunk, 0 = no split
     int64_t items = 0, combines = 0, partials = 0;
+    int group_cost = gc::kCostBuckets;  // work-list order (gc::PlanArgs)
     gc::WorkspaceLayout layout{};
 };
 
@@ -152,6 +153,8 @@ int device_cus() {
 // workgroup, or four small-tile wavefronts); otherwise cut the keys into chunks
 // (at least 512 keys, 1024 for small tiles, whose wavefronts each stream their
 // own K/V) so that the launch fills those slots.
+int64_t resident_slots(const Shape& sh) { return (sh.small ? 4LL : (sh.wide ? 1LL : 2LL)) * device_cus(); }
+
 int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
                  const gc_plan_options* o) {
     if (o != nullptr && o->kv_split_tiles != 0) return o->kv_split_tiles > 0 ? o->kv_split_tiles : 0;
@@ -166,12 +169,43 @@ int choose_chunk(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
     }
     units *= geo->num_kv_heads;
     tiles *= geo->num_kv_heads;
-    const int64_t target = (sh.small ? 4LL : (sh.wide ? 1LL : 2LL)) * device_cus();
+    const int64_t target = resident_slots(sh);
     if (units >= target || units == 0) return 0;
     int64_t chunk = (tiles + target - 1) / target;
     const int min_keys = sh.small ? 1024 : 512;
     if (chunk < min_keys / sh.block_n) chunk = min_keys / sh.block_n;
     return chunk > INT32_MAX ? 0 : (int)chunk;
+}
+
+// Work-list order. Items run in list order, and a list in strict cost order,
+// heaviest first, ends on its lightest items (longest-processing-time order).
+// Only the end needs that order, though: before it the items are sorted by the
+// length of their request instead, so that a request's query tiles, which read
+// nearly the same keys, run side by side and share the K/V tiles in L2. In cost
+// order the tiles of a long miss (one of every cost from 1 up) are spread over the
+// whole launch and each fetches the same K/V again. The lightest items, two rounds
+// of the resident slots, keep the strict order: items of fewer than group_cost
+// key tiles; a list no longer than that is not grouped at all.
+void choose_order(const gc_geometry* geo, const gc_batch* b, const Shape& sh, Plan* pl) {
+    pl->group_cost = gc::kCostBuckets;
+    const int64_t tail = (2 * resident_slots(sh) + geo->num_kv_heads - 1) / geo->num_kv_heads;  // items per KV head
+    if (pl->items <= tail) return;
+    int64_t hist[gc::kCostBuckets] = {};  // items per cost (clamped like the planner's buckets)
+    for (int r = 0; r < b->batch; ++r) {
+        const int P = b->prefix_lens_host[r], n = b->new_lens_host[r];
+        for (int q0 = 0; q0 < n; q0 += sh.tq) {
+            const int ntok = n - q0 < sh.tq ? n - q0 : sh.tq;
+            const int kt = gc::key_tiles(P, q0, ntok, sh.block_n);
+            const int ns = gc::num_splits(kt, pl->chunk);
+            const int lo = kt / ns, n_hi = kt - lo * ns;
+            hist[lo < gc::kCostBuckets - 1 ? lo : gc::kCostBuckets - 1] += ns - n_hi;
+            if (n_hi > 0) hist[lo + 1 < gc::kCostBuckets - 1 ? lo + 1 : gc::kCostBuckets - 1] += n_hi;
+        }
+    }
+    int64_t below = 0;
+    int c = 0;
+    while (c < gc::kCostBuckets && below < tail) below += hist[c++];
+    pl->group_cost = c;  // the items of cost < c make up the tail
 }
 
 gc_status make_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
@@ -188,6 +222,7 @@ gc_status make_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh,
     if (pl->items > (int64_t)INT32_MAX / geo->num_kv_heads) return GC_ERR_BAD_SHAPE;
     pl->layout = gc::workspace_layout(b->batch, pl->items, pl->combines, pl->partials,
                                       geo->num_kv_heads, geo->head_dim, sh.block_m);
+    choose_order(geo, b, sh, pl);
     return GC_OK;
 }
 
@@ -228,6 +263,7 @@ gc::PlanArgs plan_args(const gc_geometry* geo, const gc_batch* b, const Shape& s
     a.expect_partials = (int32_t)pl.partials;
     a.total_tokens = (int32_t)sh.total_tokens;
     a.max_blocks = geo->max_blocks_per_seq;
+    a.group_cost = pl.group_cost;
     return a;
 }
 

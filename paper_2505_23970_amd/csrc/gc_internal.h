@@ -159,6 +159,10 @@ struct PlanArgs {
     int32_t expect_items, expect_combines, expect_partials;
     int32_t total_tokens;     // the host's T (= cu_new_lens[batch] on the device)
     int32_t max_blocks;       // row length of the block tables
+    // Items of at least group_cost key tiles are sorted by their request's key
+    // tiles (so the items of one request stay together), lighter ones by their own
+    // cost; kCostBuckets gives the plain cost order.
+    int32_t group_cost;
 };
 
 struct AttnArgs {

@@ -9,7 +9,8 @@
 //      in the workspace), so that every thread can take query tiles of any
 //      request by a global tile index;
 //   2. a histogram of item costs (key tiles per item) in LDS, scanned so that
-//      the heaviest items come first;
+//      the heaviest items come first (above the host's cost threshold, the
+//      items of one request side by side: bucket_of);
 //   3. every item is written straight to its sorted position (an LDS cursor per
 //      cost bucket, advanced once per distinct chunk size of a tile); split query
 //      tiles take their partial slots and merge entry from two LDS counters.
@@ -56,12 +57,23 @@ __device__ int block_exclusive_scan(int v, int* s_tmp, int* total) {
     return base + x - v;
 }
 
-__device__ __forceinline__ int bucket_of(int cost) {
-    return kCostBuckets - 1 - min(cost, kCostBuckets - 1);  // heaviest first
+// Counting-sort bucket of an item of `cost` key tiles from a request of
+// `req_tiles` key tiles in all. Items of at least group_cost key tiles are sorted
+// by req_tiles, longest request first, so that all of a request's items run side
+// by side: its query tiles read nearly the same keys and share them in L2, where
+// in cost order the tiles of one request (a long miss has tiles of every cost
+// from 1 up) are spread over the launch and fetch the same K/V again each time.
+// Lighter items, the last rounds of the launch, follow in cost order, heaviest
+// first, so that the launch still ends on its lightest items. req_tiles >= cost,
+// so every grouped item precedes every lighter one.
+__device__ __forceinline__ int bucket_of(const PlanArgs& a, int cost, int req_tiles) {
+    const int c = min(cost, kCostBuckets - 1);
+    return kCostBuckets - 1 - (c >= a.group_cost ? min(req_tiles, kCostBuckets - 1) : c);
 }
 
 struct Tile {
     int r, q0, kt, ns;
+    int req_tiles;  // key tiles of the whole request
 };
 
 // Batch lengths as the planner reads them: LDS copies for batches of up to
@@ -88,6 +100,7 @@ __device__ __forceinline__ Tile tile_at(const PlanArgs& a, const Lens& l, int g)
     const int ntok = min(a.tq, n - t.q0);
     t.kt = key_tiles(l.prefix[lo], t.q0, ntok, a.block_n);
     t.ns = num_splits(t.kt, a.chunk);
+    t.req_tiles = key_tiles(l.prefix[lo], 0, n, a.block_n);
     return t;
 }
 
@@ -169,8 +182,8 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, PlanLds& sm) {
     for (int g = tid; g < total_tiles; g += kPlanThreads) {
         const Tile t = tile_at(a, lens, g);
         const int lo = t.kt / t.ns, n_hi = t.kt - lo * t.ns, n_lo = t.ns - n_hi;
-        if (n_lo > 0) atomicAdd(&s_hist[bucket_of(lo)], n_lo);
-        if (n_hi > 0) atomicAdd(&s_hist[bucket_of(lo + 1)], n_hi);
+        if (n_lo > 0) atomicAdd(&s_hist[bucket_of(a, lo, t.req_tiles)], n_lo);
+        if (n_hi > 0) atomicAdd(&s_hist[bucket_of(a, lo + 1, t.req_tiles)], n_hi);
     }
     __syncthreads();
     constexpr int kPer = kCostBuckets / kPlanThreads;
@@ -209,8 +222,8 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, PlanLds& sm) {
         }
         // reserve the tile's positions in both cost buckets at once, then hand them out
         const int lo = t.kt / t.ns, n_hi = t.kt - lo * t.ns, n_lo = t.ns - n_hi;
-        int pos_lo = n_lo > 0 ? atomicAdd(&s_hist[bucket_of(lo)], n_lo) : 0;
-        int pos_hi = n_hi > 0 ? atomicAdd(&s_hist[bucket_of(lo + 1)], n_hi) : 0;
+        int pos_lo = n_lo > 0 ? atomicAdd(&s_hist[bucket_of(a, lo, t.req_tiles)], n_lo) : 0;
+        int pos_hi = n_hi > 0 ? atomicAdd(&s_hist[bucket_of(a, lo + 1, t.req_tiles)], n_hi) : 0;
         for (int s = 0; s < t.ns; ++s) {
             const int b0 = split_begin(s, t.kt, t.ns), b1 = split_begin(s + 1, t.kt, t.ns);
             const int pos = b1 - b0 == lo ? pos_lo++ : pos_hi++;
