@@ -138,6 +138,10 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     const int lr = lane & 31;
     const int kvh = (int)(blockIdx.x % (unsigned)a.num_kv_heads);
     const WorkItem it = a.items[blockIdx.x / (unsigned)a.num_kv_heads];
+    // all eight fields in one load (else the fields the test below needs are loaded
+    // first and the rest after it, a second dependent round trip)
+    asm volatile("" ::"s"(it.r), "s"(it.q0), "s"(it.kt_begin), "s"(it.kt_end), "s"(it.part), "s"(it.P),
+                 "s"(it.cu), "s"(it.n));
     if (it.r < 0 || it.kt_begin >= it.kt_end) return;
 
     // (the planner repeats the request's lengths in the item: one load for all of them)
@@ -155,6 +159,12 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     const bool row_ok = t < ntok;
     const int lim = P + it.q0 + (row_ok ? t : 0);  // last key this row may see
     const int64_t qrow = (int64_t)(cu + it.q0 + t) * a.num_q_heads + kvh * a.group + hl;
+
+    // block-table entries of the first key tile, loaded before Q: loads return in
+    // order, so the first tile's copies then wait for these entries only and go out
+    // while Q is still in flight (entry p in lanes with lane % 4 == p; clamped into
+    // the row, checked at use)
+    int ids = a.block_tables[(int64_t)r * a.max_blocks + min(it.kt_begin * 4 + (lane & 3), a.max_blocks - 1)];
 
     // Q^T operand: lane holds q[row][16k + 8*hh .. +7]
     bf16x8 qf[DK];
@@ -567,7 +577,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
 
     // One pipeline step: start the next tile's loads into the other buffers, compute
     // this tile, make the next tile visible.
-    int ids;        // block-table entries of the next tile to copy (entry p in lanes with lane % 4 == p)
+    // (ids: block-table entries of the next tile to copy, entry p in lanes with lane % 4 == p)
     int bl_cur[4];  // (fused append) the entries of the tile being computed, wave-uniform
     auto take_ids = [&](int (&bl)[4]) {
 #pragma unroll
@@ -626,7 +636,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     l_run = 0.f;
     l_run1 = 0.f;
     kt = it.kt_begin;
-    fetch_ids(kt, ids);
+    if (exact) fetch_ids(kt, ids);  // the first pass has them from the start
     if constexpr (FP8) {
         load8(kt, ids);
         if (kt + 1 < it.kt_end) fetch_ids(kt + 1, ids);
