@@ -223,11 +223,28 @@ def measured_mfma_tflops(iterations=4000, reps=5):
     return flops / t / 1e12
 
 
+def traffic_sources(kernel_source):
+    """Sources that decide an attention launch's memory traffic: the kernel's file, the
+    planner that orders its work items and the host policy that picks the tiling,
+    key split and order (and the shared definitions)."""
+    return [kernel_source, "paper_2505_23970_amd/csrc/plan_body.h", "paper_2505_23970_amd/csrc/api.hip",
+            "paper_2505_23970_amd/csrc/gc_internal.h"]
+
+
+def sources_sha256_16(paths):
+    """First 16 hex digits of the SHA-256 of the files' contents, concatenated in order."""
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
 def profiled_traffic(workload):
     """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary of this workload, if it was taken on the current source of the profiled
-    kernel; else None."""
-    import hashlib
+    summary of this workload, if it was taken on the current sources of the profiled
+    kernel and its planner; else None."""
     path = os.path.join(ROOT, "profiles", f"attention_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -236,14 +253,12 @@ def profiled_traffic(workload):
         for line in f:
             if line.startswith("traffic-json:"):
                 rec = json.loads(line.split(":", 1)[1])
-    if rec is None:
+    if rec is None or not rec.get("kernel_sources"):
         return None
-    src = os.path.join(ROOT, rec.get("kernel_source", "paper_2505_23970_amd/csrc/attention.hip"))
-    if not os.path.exists(src):
+    srcs = rec["kernel_sources"]
+    if not all(os.path.exists(os.path.join(ROOT, p)) for p in srcs):
         return None
-    with open(src, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    return rec["traffic_bytes"] if rec.get("kernel_source_sha256_16") == sha else None
+    return rec["traffic_bytes"] if rec.get("sources_sha256_16") == sources_sha256_16(srcs) else None
 
 
 def cpu_oracle_baseline(w, target_s, fp8=None):

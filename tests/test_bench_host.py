@@ -46,16 +46,19 @@ def test_attention_bytes_read_kv_once_and_q_o_once():
 
 def test_profiled_traffic_follows_the_committed_profile():
     """The traffic figure comes from the profile's traffic-json line and only while
-    the profiled kernel source is unchanged."""
+    the profiled kernel's sources (kernel, planner, host policy) are unchanged."""
     path = os.path.join(ROOT, "profiles", "attention_llama3_8b.md")
     rec = None
     for line in open(path):
         if line.startswith("traffic-json:"):
             rec = json.loads(line.split(":", 1)[1])
     assert rec is not None and rec["traffic_bytes"] == rec["fetch_bytes"] + rec["write_bytes"]
-    sha = hashlib.sha256(open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()).hexdigest()[:16]
+    assert rec["kernel_sources"] == bench.traffic_sources(rec["kernel_sources"][0])
+    h = hashlib.sha256()
+    for p in rec["kernel_sources"]:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
     got = bench.profiled_traffic("llama3_8b")
-    if sha == rec["kernel_source_sha256_16"]:
+    if h.hexdigest()[:16] == rec["sources_sha256_16"]:
         assert got == rec["traffic_bytes"]
         # HBM traffic of one launch is at least the bytes the kernel must write (O)
         w = bench.WORKLOADS["llama3_8b"]()
