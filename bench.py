@@ -231,20 +231,47 @@ def traffic_sources(kernel_source):
             "paper_2505_23970_amd/csrc/gc_internal.h"]
 
 
-def sources_sha256_16(paths):
-    """First 16 hex digits of the SHA-256 of the files' contents, concatenated in order."""
+def code_text(text):
+    """A C/C++/HIP source without its comments, whitespace runs collapsed to one space
+    (string and character literals kept as they are)."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
+def code_sha256_16(paths):
+    """First 16 hex digits of the SHA-256 of the files' code (code_text), in order: a
+    comment-only edit keeps it, any change to the code changes it."""
     import hashlib
     h = hashlib.sha256()
     for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+            h.update(code_text(f.read()).encode())
+        h.update(b"\0")
     return h.hexdigest()[:16]
 
 
 def profiled_traffic(workload):
     """HBM bytes per attention launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    summary of this workload, if it was taken on the current sources of the profiled
-    kernel and its planner; else None."""
+    summary of this workload, if it was taken on the current code of the profiled kernel
+    and its planner (comments aside); else None."""
     path = os.path.join(ROOT, "profiles", f"attention_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -258,7 +285,7 @@ def profiled_traffic(workload):
     srcs = rec["kernel_sources"]
     if not all(os.path.exists(os.path.join(ROOT, p)) for p in srcs):
         return None
-    return rec["traffic_bytes"] if rec.get("sources_sha256_16") == sources_sha256_16(srcs) else None
+    return rec["traffic_bytes"] if rec.get("code_sha256_16") == code_sha256_16(srcs) else None
 
 
 def cpu_oracle_baseline(w, target_s, fp8=None):

@@ -152,7 +152,7 @@ struct PlanArgs {
     const int32_t* cu_new_lens;
     int32_t* scratch;         // 3 * (batch + 1) int32
     WorkItem* unsorted;       // [items]
-    WorkItem* items;          // [items], sorted by cost, heaviest first
+    WorkItem* items;          // [items], in launch order (see group_cost)
     CombineItem* combines;    // [combines]
     int32_t* status;          // status[0] = 0 when the device lengths matched the host's
     int32_t batch, tq, chunk, block_n;

@@ -14,10 +14,12 @@
 //   3. every item is written straight to its sorted position (an LDS cursor per
 //      cost bucket, advanced once per distinct chunk size of a tile); split query
 //      tiles take their partial slots and merge entry from two LDS counters.
-// The hardware dispatcher starts workgroups in index order, so the longest
-// items start first (longest-processing-time scheduling). Order inside a cost
-// bucket and slot numbers may differ between runs; results do not depend on
-// them (every item writes its own outputs, merges run in chunk order).
+// The hardware dispatcher starts workgroups in index order: the items of the
+// longest requests start first, each request's items together, and the launch
+// ends on its lightest items in cost order (longest-processing-time scheduling
+// where it matters, at the end). Order inside a bucket and slot numbers may
+// differ between runs; results do not depend on them (every item writes its own
+// outputs, merges run in chunk order).
 // The device lengths are checked before anything is derived from them: cu[0]
 // must be 0, cu non-decreasing with cu[B] equal to the host's T, every prefix
 // length non-negative, every request's keys within the block-table row, and the

@@ -46,7 +46,7 @@ def test_attention_bytes_read_kv_once_and_q_o_once():
 
 def test_profiled_traffic_follows_the_committed_profile():
     """The traffic figure comes from the profile's traffic-json line and only while
-    the profiled kernel's sources (kernel, planner, host policy) are unchanged."""
+    the profiled kernel's code (kernel, planner, host policy) is unchanged."""
     path = os.path.join(ROOT, "profiles", "attention_llama3_8b.md")
     rec = None
     for line in open(path):
@@ -54,17 +54,31 @@ def test_profiled_traffic_follows_the_committed_profile():
             rec = json.loads(line.split(":", 1)[1])
     assert rec is not None and rec["traffic_bytes"] == rec["fetch_bytes"] + rec["write_bytes"]
     assert rec["kernel_sources"] == bench.traffic_sources(rec["kernel_sources"][0])
-    h = hashlib.sha256()
-    for p in rec["kernel_sources"]:
-        h.update(open(os.path.join(ROOT, p), "rb").read())
     got = bench.profiled_traffic("llama3_8b")
-    if h.hexdigest()[:16] == rec["sources_sha256_16"]:
+    if bench.code_sha256_16(rec["kernel_sources"]) == rec["code_sha256_16"]:
         assert got == rec["traffic_bytes"]
         # HBM traffic of one launch is at least the bytes the kernel must write (O)
         w = bench.WORKLOADS["llama3_8b"]()
         assert got >= 2 * w.total_new * w.num_q_heads * w.head_dim
     else:
         assert got is None
+
+
+def test_code_hash_ignores_comments_and_layout_only(tmp_path):
+    files = {
+        "a.hip": "int f(int x) { return x + 1; } // one\n",
+        "b.hip": "/* a header */\nint f(int x)  {\n    return x + 1;  // another\n}\n",
+        "c.hip": "int f(int x) { return x + 2; }\n",
+        "d.hip": 'const char* p = "// kept"; char q = \'/\';\n',
+        "e.hip": 'const char* p = "// changed"; char q = \'/\';\n',
+    }
+    for name, text in files.items():
+        (tmp_path / name).write_text(text)
+    h = {name: bench.code_sha256_16([str(tmp_path / name)]) for name in files}
+    assert h["a.hip"] == h["b.hip"]
+    assert h["a.hip"] != h["c.hip"]
+    assert h["d.hip"] != h["e.hip"]  # text inside a string literal is code
+    assert bench.code_text(files["d.hip"]) == 'const char* p = "// kept"; char q = \'/\';'
     assert bench.profiled_traffic("no_such_workload") is None
 
 
