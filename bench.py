@@ -180,7 +180,28 @@ def auto_kernel_name(w, cus, fp8):
     rows = int(w.new_lens.sum()) * g
     grid = units * w.num_kv_heads
     wide = rows * 100 >= units * 256 * 85 and not (cus < grid < 2 * cus)
+    if wide and not fp8 and cus % 8 == 0 and wide_items(w, cus) * w.num_kv_heads >= 4 * cus:
+        # resident launch: one workgroup per CU taking the items from per-XCD queues
+        return f"attention_resident_kernel<{D}> (+ split merge when the plan splits)"
     return f"attention_kernel<{D}, {8 if wide else 4}{f}> (+ split merge when the plan splits)"
+
+
+def wide_items(w, cus):
+    """Work items per KV head of the wide tiling (query tiles of 256 rows, cut into key
+    chunks when they do not fill one workgroup per compute unit: the split rule of
+    choose_chunk in the C ABI, restated)."""
+    g = w.num_q_heads // w.num_kv_heads
+    tq = 256 // g
+    tiles = []
+    for P, n in zip(w.prefix_lens, w.new_lens):
+        for q0 in range(0, int(n), tq):
+            ntok = min(tq, int(n) - q0)
+            tiles.append((int(P) + q0 + ntok + 63) // 64)
+    units = len(tiles) * w.num_kv_heads
+    if units == 0 or units >= cus:
+        return len(tiles)
+    chunk = max((sum(tiles) * w.num_kv_heads + cus - 1) // cus, 512 // 64)
+    return sum(1 if kt <= chunk else (kt + chunk - 1) // chunk for kt in tiles)
 
 
 def measured_read_gbs(mib=4096, reps=5):

@@ -180,6 +180,9 @@ gc_status gc_prefix_prefill_plan_status(const void* workspace, size_t workspace_
  *   out   : device bf16 [T][Hq][D], rounded to nearest even
  *   lse   : device fp32 [T][Hq] natural-log log-sum-exp, or NULL
  * The pools must already hold every key of every request (prefix and new).
+ * The workspace also holds state that runs update (split-KV partials, and the work
+ * queues of large wide-tile launches, which the plan clears and every run leaves
+ * cleared): runs that share a workspace must be ordered (one stream, or waited for).
  */
 gc_status gc_prefix_prefill_run(const gc_geometry* geo, const gc_batch* batch,
                                 const gc_plan_options* opts,

@@ -254,6 +254,7 @@ gc::PlanArgs plan_args(const gc_geometry* geo, const gc_batch* b, const Shape& s
     a.items = at<gc::WorkItem>(ws, pl.layout.items_off);
     a.combines = at<gc::CombineItem>(ws, pl.layout.combine_off);
     a.status = at<int32_t>(ws, pl.layout.status_off);
+    a.queues = at<int32_t>(ws, pl.layout.queue_off);
     a.batch = b->batch;
     a.tq = sh.tq;
     a.chunk = pl.chunk;
@@ -270,6 +271,18 @@ gc::PlanArgs plan_args(const gc_geometry* geo, const gc_batch* b, const Shape& s
 gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& sh, const Plan& pl,
                        void* ws, hipStream_t stream) {
     return gc::launch_plan(plan_args(geo, b, sh, pl, ws), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
+}
+
+// Wide tiles over bf16 pools with at least four rounds of work items per compute unit
+// run as a resident launch (one workgroup per CU taking items from per-XCD queues;
+// attention.hip): it removes the dispatch gaps between items and lets the XCDs that
+// finish first take the last items of the others. With fewer rounds the tickets cost
+// more than they save. 0: the regular launch.
+int resident_workgroups(const gc_geometry* geo, const Shape& sh, const Plan& pl, bool fp8) {
+    if (!sh.wide || fp8) return 0;
+    const int cus = device_cus();
+    if (cus % gc::kQueues != 0) return 0;
+    return pl.items * geo->num_kv_heads >= 4LL * cus ? cus : 0;
 }
 
 // Pools of bf16 elements (fp8 false, scales 1) or of E4M3 codes with one scale each.
@@ -294,6 +307,7 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
     a.cu_new_lens = b->cu_new_lens_dev;
     a.block_tables = b->block_tables_dev;
     a.items = at<gc::WorkItem>(ws, pl.layout.items_off);
+    a.queues = at<int32_t>(ws, pl.layout.queue_off);
     a.num_q_heads = geo->num_q_heads;
     a.num_kv_heads = geo->num_kv_heads;
     a.group = sh.group;
@@ -311,7 +325,8 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
         e = gc::launch_attention_append(a, geo->head_dim, pl.items, sh.wide, stream);
     } else {
         e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, pk.fp8, stream)
-                     : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, pk.fp8, stream);
+                     : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, pk.fp8,
+                                            resident_workgroups(geo, sh, pl, pk.fp8), stream);
     }
     if (e != hipSuccess) return GC_ERR_HIP;
     if (pl.combines > 0) {

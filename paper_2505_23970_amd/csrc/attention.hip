@@ -107,11 +107,12 @@ __device__ __forceinline__ void widen_e4m3x16(const u32x4 c, u32x4& lo, u32x4& h
     hi = u32x4{w[4], w[5], w[6], w[7]};
 }
 
-// One work item (a workgroup of WAVES wavefronts). FUSE: the KV append runs in the
+// One work item (a workgroup of WAVES wavefronts): the item of launch index bid
+// (blockIdx.x in the regular launch), i.e. work item bid / Hkv for KV head bid % Hkv. FUSE: the KV append runs in the
 // same launch, so the keys at or past the prefix length are taken from the new
 // tokens' arrays, not from the pool (bf16 pools only).
 template <int D, int WAVES, bool FP8, bool FUSE>
-__device__ __forceinline__ void attention_body(const AttnArgs& a) {
+__device__ __forceinline__ void attention_body(const AttnArgs& a, const unsigned bid) {
     static_assert(!(FP8 && FUSE), "the fused append runs over bf16 pools");
     constexpr int kBlockRows = WAVES * kRowsPerWave;  // query rows of a work item
     constexpr int DK = D / 16;                      // k-steps of QK^T
@@ -136,8 +137,8 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hh = lane >> 5;
     const int lr = lane & 31;
-    const int kvh = (int)(blockIdx.x % (unsigned)a.num_kv_heads);
-    const WorkItem it = a.items[blockIdx.x / (unsigned)a.num_kv_heads];
+    const int kvh = (int)(bid % (unsigned)a.num_kv_heads);
+    const WorkItem it = a.items[bid / (unsigned)a.num_kv_heads];
     // all eight fields in one load (else the fields the test below needs are loaded
     // first and the rest after it, a second dependent round trip)
     asm volatile("" ::"s"(it.r), "s"(it.q0), "s"(it.kt_begin), "s"(it.kt_end), "s"(it.part), "s"(it.P),
@@ -750,7 +751,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a) {
 
 template <int D, int WAVES, bool FP8>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const AttnArgs a) {
-    attention_body<D, WAVES, FP8, false>(a);
+    attention_body<D, WAVES, FP8, false>(a, blockIdx.x);
 }
 
 // Attention with the KV append fused in: the work items read new keys from the new
@@ -758,12 +759,56 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_kernel(const 
 // keys and values into the pools from LDS.
 template <int D, int WAVES>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_append_kernel(const AttnArgs a) {
-    attention_body<D, WAVES, false, true>(a);
+    attention_body<D, WAVES, false, true>(a, blockIdx.x);
 }
 
 // Merge the key chunks of one split query tile: with m = max_s lse_s,
 // lse = m + log sum_s exp(lse_s - m) and o = sum_s exp(lse_s - m) o_s / sum_s exp(lse_s - m),
 // in a fixed chunk order (deterministic).
+
+// Resident launch (wide tiles over bf16 pools): one workgroup per compute unit, each
+// taking work items until none is left. Queue x holds the regular launch's indices
+// x, x + 8, x + 16, ...: the hardware deals workgroups to the eight XCDs in turn, so
+// workgroup b serves queue b % 8 and each XCD runs the items (and KV heads) it runs in
+// the regular launch, keeping their K/V in its L2. A workgroup whose queue is empty
+// takes items from the other queues, so XCDs that run slower do not hold up the end of
+// the launch; and a freed compute unit starts its next item without waiting for the
+// dispatcher, which hands out new workgroups in index order across the XCDs. Tickets
+// are agent-scope atomics on the workspace's counters; the last workgroup to leave
+// sets them back to zero for the next launch (the ticket atomics of every other
+// workgroup returned before it counted itself out).
+template <int D>
+__global__ __launch_bounds__(kWideWaves * 64, 1) void attention_resident_kernel(const AttnArgs a, int total) {
+    __shared__ int s_tk, s_empty;
+    const int x = (int)(blockIdx.x % (unsigned)kQueues);
+    if (threadIdx.x == 0) s_empty = 0;
+    for (;;) {
+        if (threadIdx.x == 0) {
+            int b = -1, empty = s_empty;
+            for (int j = 0; j < kQueues && b < 0; ++j) {
+                const int y = (x + j) % kQueues;
+                if (empty & (1 << y)) continue;
+                const int k = __hip_atomic_fetch_add(&a.queues[y], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((int64_t)k * kQueues + y < total) b = k * kQueues + y;
+                else empty |= 1 << y;
+            }
+            s_empty = empty;
+            s_tk = b;
+        }
+        __syncthreads();
+        const int b = s_tk;
+        __syncthreads();  // every wavefront has read the ticket before the next one is written
+        if (b < 0) break;
+        attention_body<D, kWideWaves, false, false>(a, (unsigned)b);
+    }
+    if (threadIdx.x == 0) {
+        const int out = __hip_atomic_fetch_add(&a.queues[kQueues], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (out == (int)gridDim.x - 1)
+            for (int y = 0; y <= kQueues; ++y)
+                __hip_atomic_store(&a.queues[y], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 // A workgroup merges kCombineRows rows of one (query tile, KV head); a thread
 // owns four consecutive output elements of one row, so the partial rows are
 // read with coalesced 16-byte loads.
@@ -848,8 +893,18 @@ static void launch_prefill(const AttnArgs& a, int head_dim, const dim3 grid, boo
 }
 
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
-                            hipStream_t s) {
+                            int resident, hipStream_t s) {
     const dim3 grid((unsigned)(num_items * a.num_kv_heads));
+    if (resident > 0 && wide && !fp8) {
+        const int total = (int)(num_items * a.num_kv_heads);
+        if (head_dim == 128)
+            hipLaunchKernelGGL(attention_resident_kernel<128>, dim3((unsigned)resident), dim3(kWideWaves * 64), 0, s,
+                               a, total);
+        else
+            hipLaunchKernelGGL(attention_resident_kernel<64>, dim3((unsigned)resident), dim3(kWideWaves * 64), 0, s,
+                               a, total);
+        return hipGetLastError();
+    }
     if (fp8)
         launch_prefill<true>(a, head_dim, grid, wide, s);
     else

@@ -105,9 +105,14 @@ __host__ __device__ inline RequestCounts request_counts(int prefix, int n, int t
 
 // ---------------------------------------------------------------- workspace
 constexpr size_t kStatusOffset = 0;  // byte offset of the planner's status word in the workspace
+// Work queues of the resident attention launch: kQueues ticket counters and one exit
+// counter (int32) in the workspace's leading 256-byte block, zeroed by the planner and
+// left at zero by every launch that uses them.
+constexpr size_t kQueueOffset = 64;
+constexpr int kQueues = 8;  // one per XCD
 
 struct WorkspaceLayout {
-    size_t items_off, combine_off, scratch_off, part_lse_off, part_o_off, status_off, total;
+    size_t items_off, combine_off, scratch_off, part_lse_off, part_o_off, status_off, queue_off, total;
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -117,6 +122,7 @@ inline WorkspaceLayout workspace_layout(int batch, int64_t items, int64_t combin
     WorkspaceLayout w{};
     size_t off = kStatusOffset;
     w.status_off = off;
+    w.queue_off = off + kQueueOffset;
     off = align_up(off + 256, 256);
     w.items_off = off;
     off = align_up(off + sizeof(WorkItem) * (size_t)(items > 0 ? items : 1), 256);
@@ -155,6 +161,7 @@ struct PlanArgs {
     WorkItem* items;          // [items], in launch order (see group_cost)
     CombineItem* combines;    // [combines]
     int32_t* status;          // status[0] = 0 when the device lengths matched the host's
+    int32_t* queues;          // [kQueues + 1] work-queue counters, zeroed here
     int32_t batch, tq, chunk, block_n;
     int32_t expect_items, expect_combines, expect_partials;
     int32_t total_tokens;     // the host's T (= cu_new_lens[batch] on the device)
@@ -177,6 +184,7 @@ struct AttnArgs {
     const int32_t* cu_new_lens;
     const int32_t* block_tables;
     const WorkItem* items;
+    int32_t* queues;     // resident launch: [kQueues] ticket counters, then the exit counter
     int32_t num_q_heads, num_kv_heads, group, tq;
     int32_t num_blocks, max_blocks;
     float scale_log2;    // softmax scale * log2(e) (times the key scale for 8-bit pools)
@@ -207,8 +215,10 @@ hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 // append (AppendArgs) and plan (PlanArgs) in one launch
 hipError_t launch_prepare(const AppendArgs& aa, const PlanArgs& pa, int head_dim, bool fp8, hipStream_t s);
+// resident > 0 (wide tiles over bf16 pools only): that many resident workgroups take
+// the items from the work queues instead of one workgroup per item
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
-                            hipStream_t s);
+                            int resident, hipStream_t s);
 // attention with the KV append fused in (AttnArgs with k_new, v_new, k_dst, v_dst
 // set); prefill tiles over bf16 pools
 hipError_t launch_attention_append(const AttnArgs& a, int head_dim, int64_t num_items, bool wide,

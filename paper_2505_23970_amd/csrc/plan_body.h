@@ -127,6 +127,7 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, PlanLds& sm) {
     int* const s_cu = sm.cu;
     int* const s_pre = sm.pre;
     const int tid = threadIdx.x;
+    if (tid <= kQueues) a.queues[tid] = 0;  // the resident attention launch starts from empty tickets
     const bool small = a.batch <= kPlanLdsBatch;
     int* cum = small ? s_cum : a.scratch;  // [batch + 1]
     if (tid == 0) s_badlen = 0;
