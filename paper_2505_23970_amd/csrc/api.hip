@@ -273,13 +273,13 @@ gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& s
     return gc::launch_plan(plan_args(geo, b, sh, pl, ws), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
 }
 
-// Wide tiles over bf16 pools with at least four rounds of work items per compute unit
+// Wide tiles with at least four rounds of work items per compute unit
 // run as a resident launch (one workgroup per CU taking items from per-XCD queues;
 // attention.hip): it removes the dispatch gaps between items and lets the XCDs that
 // finish first take the last items of the others. With fewer rounds the tickets cost
 // more than they save. 0: the regular launch.
-int resident_workgroups(const gc_geometry* geo, const Shape& sh, const Plan& pl, bool fp8) {
-    if (!sh.wide || fp8) return 0;
+int resident_workgroups(const gc_geometry* geo, const Shape& sh, const Plan& pl) {
+    if (!sh.wide) return 0;
     const int cus = device_cus();
     if (cus % gc::kQueues != 0) return 0;
     return pl.items * geo->num_kv_heads >= 4LL * cus ? cus : 0;
@@ -326,7 +326,7 @@ gc_status enqueue_run(const gc_geometry* geo, const gc_batch* b, const Shape& sh
     } else {
         e = sh.small ? gc::launch_attention_small(a, geo->head_dim, pl.items, pk.fp8, stream)
                      : gc::launch_attention(a, geo->head_dim, pl.items, sh.wide, pk.fp8,
-                                            resident_workgroups(geo, sh, pl, pk.fp8), stream);
+                                            resident_workgroups(geo, sh, pl), stream);
     }
     if (e != hipSuccess) return GC_ERR_HIP;
     if (pl.combines > 0) {

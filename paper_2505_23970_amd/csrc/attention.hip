@@ -132,7 +132,12 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a, const unsigned
     __shared__ __align__(16) unsigned char k_lds1[kTileBytes];
     __shared__ __align__(16) unsigned char v_lds1[kTileBytes];
 
-    const int tid = threadIdx.x;
+    // (opaque to the compiler, so that the lane constants derived from it are computed per
+    // work item: hoisted out of the resident launch's item loop they would be held, or
+    // spilled, across the tile loop)
+    int tid_opaque = (int)threadIdx.x;
+    asm volatile("" : "+v"(tid_opaque));
+    const int tid = tid_opaque;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hh = lane >> 5;
@@ -766,7 +771,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_append_kernel
 // lse = m + log sum_s exp(lse_s - m) and o = sum_s exp(lse_s - m) o_s / sum_s exp(lse_s - m),
 // in a fixed chunk order (deterministic).
 
-// Resident launch (wide tiles over bf16 pools): one workgroup per compute unit, each
+// Resident launch (wide tiles): one workgroup per compute unit, each
 // taking work items until none is left. Queue x holds the regular launch's indices
 // x, x + 8, x + 16, ...: the hardware deals workgroups to the eight XCDs in turn, so
 // workgroup b serves queue b % 8 and each XCD runs the items (and KV heads) it runs in
@@ -777,7 +782,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void attention_append_kernel
 // are agent-scope atomics on the workspace's counters; the last workgroup to leave
 // sets them back to zero for the next launch (the ticket atomics of every other
 // workgroup returned before it counted itself out).
-template <int D>
+template <int D, bool FP8>
 __global__ __launch_bounds__(kWideWaves * 64, 1) void attention_resident_kernel(const AttnArgs a, int total) {
     __shared__ int s_tk, s_empty;
     const int x = (int)(blockIdx.x % (unsigned)kQueues);
@@ -799,7 +804,7 @@ __global__ __launch_bounds__(kWideWaves * 64, 1) void attention_resident_kernel(
         const int b = s_tk;
         __syncthreads();  // every wavefront has read the ticket before the next one is written
         if (b < 0) break;
-        attention_body<D, kWideWaves, false, false>(a, (unsigned)b);
+        attention_body<D, kWideWaves, FP8, false>(a, (unsigned)b);
     }
     if (threadIdx.x == 0) {
         const int out = __hip_atomic_fetch_add(&a.queues[kQueues], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -895,14 +900,16 @@ static void launch_prefill(const AttnArgs& a, int head_dim, const dim3 grid, boo
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
                             int resident, hipStream_t s) {
     const dim3 grid((unsigned)(num_items * a.num_kv_heads));
-    if (resident > 0 && wide && !fp8) {
+    if (resident > 0 && wide) {
         const int total = (int)(num_items * a.num_kv_heads);
-        if (head_dim == 128)
-            hipLaunchKernelGGL(attention_resident_kernel<128>, dim3((unsigned)resident), dim3(kWideWaves * 64), 0, s,
-                               a, total);
-        else
-            hipLaunchKernelGGL(attention_resident_kernel<64>, dim3((unsigned)resident), dim3(kWideWaves * 64), 0, s,
-                               a, total);
+        const dim3 rg((unsigned)resident), rb(kWideWaves * 64);
+        if (head_dim == 128) {
+            if (fp8) hipLaunchKernelGGL((attention_resident_kernel<128, true>), rg, rb, 0, s, a, total);
+            else hipLaunchKernelGGL((attention_resident_kernel<128, false>), rg, rb, 0, s, a, total);
+        } else {
+            if (fp8) hipLaunchKernelGGL((attention_resident_kernel<64, true>), rg, rb, 0, s, a, total);
+            else hipLaunchKernelGGL((attention_resident_kernel<64, false>), rg, rb, 0, s, a, total);
+        }
         return hipGetLastError();
     }
     if (fp8)

@@ -215,7 +215,7 @@ hipError_t launch_append(const AppendArgs& a, int head_dim, bool fp8, hipStream_
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 // append (AppendArgs) and plan (PlanArgs) in one launch
 hipError_t launch_prepare(const AppendArgs& aa, const PlanArgs& pa, int head_dim, bool fp8, hipStream_t s);
-// resident > 0 (wide tiles over bf16 pools only): that many resident workgroups take
+// resident > 0 (wide tiles only): that many resident workgroups take
 // the items from the work queues instead of one workgroup per item
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
                             int resident, hipStream_t s);

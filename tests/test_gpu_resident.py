@@ -1,5 +1,5 @@
-"""Resident attention launch (GPU): wide tiles over bf16 pools with at least four rounds
-of work items per compute unit run as one workgroup per CU taking items from per-XCD
+"""Resident attention launch (GPU): wide tiles (bf16 or 8-bit pools) with at least four
+rounds of work items per compute unit run as one workgroup per CU taking items from per-XCD
 ticket queues in the workspace. The queues must start empty after every plan and be
 left empty by every run, whatever the workspace held before."""
 import sys
@@ -29,26 +29,27 @@ def gpu_ready():
     gc.load_library()
 
 
-def resident_batch(seed):
+def resident_batch(seed, D=128):
     # 64 q / 8 kv heads: wide tiles of 32 tokens; 4 misses of 1024 tokens and two hits
     # give 139 work items per KV head, 1112 workgroups: more than four per CU
-    return W.build([0, 0, 0, 0, 2000, 3000], [1024, 1024, 1024, 1024, 200, 100], 64, 8, 128,
-                   seed=seed, name=f"resident_{seed}")
+    return W.build([0, 0, 0, 0, 2000, 3000], [1024, 1024, 1024, 1024, 200, 100], 64, 8, D,
+                   seed=seed, name=f"resident_{seed}_d{D}")
 
 
-def test_resident_runs_repeat_bitwise_and_match_the_oracle():
+@pytest.mark.parametrize("D", [64, 128])
+def test_resident_runs_repeat_bitwise_and_match_the_oracle(D):
     import torch
     import paper_2505_23970_amd as gc
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    w = resident_batch(301)
+    w = resident_batch(301, D)
     items = sum(-(-int(n) // 32) for n in w.new_lens)
     if cus % 8 != 0 or items * w.num_kv_heads < 4 * cus:
         pytest.skip(f"{items * w.num_kv_heads} workgroups do not make four rounds on {cus} CUs")
-    say(f"case resident_301: {items} items per KV head, {cus} CUs")
+    say(f"case {w.name}: {items} items per KV head, {cus} CUs")
     kp_ref, vp_ref = H.oracle_pools(w)
     run = H.DeviceRun(w)
     run.append()
-    T, Hq, D = w.q.shape
+    T, Hq, _ = w.q.shape
     ws = gc.alloc_workspace(Hq, run.k_pool, run.v_pool, run.batch)
     ws[QUEUE_BYTES[0]:QUEUE_BYTES[1]] = 0x7F  # left-over counters: the plan must clear them
     gc.plan(Hq, run.k_pool, run.v_pool, run.batch, ws)
@@ -104,3 +105,40 @@ def test_resident_runs_on_two_workspaces_interleaved():
         out = torch.from_numpy(outs[k].view(np.int16)).view(torch.bfloat16)
         info = H.compare_attention(w, out, None, ref_out, None, rows=rows, contract=True)
         say(f"workspace {k}: {info}")
+
+
+@pytest.mark.parametrize("D", [64, 128])
+def test_resident_launch_over_8bit_pools(D):
+    """The resident launch over 8-bit pools (each head dimension its own kernel
+    instance): two runs on one plan bitwise equal, sampled rows against the oracle's
+    dequantised attention."""
+    import torch
+    import paper_2505_23970_amd as gc
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    w = W.build([0, 0, 0, 0, 2000, 3000], [1024, 1024, 1024, 1024, 200, 100], 64, 8, D,
+                seed=310 + D, name=f"resident_fp8_d{D}")
+    items = sum(-(-int(n) // 32) for n in w.new_lens)
+    if cus % 8 != 0 or items * w.num_kv_heads < 4 * cus:
+        pytest.skip("not a resident launch on this GPU")
+    ks, vs = 2.0 ** -6, 0.0213
+    say(f"case {w.name}: 8-bit pools, {items} items per KV head")
+    run = H.DeviceRunFp8(w, ks, vs)
+    run.append()
+    kref, vref = H.oracle_pools_fp8(run)
+    T, Hq, _ = w.q.shape
+    ws = gc.alloc_workspace(Hq, run.k_pool, run.v_pool, run.batch)
+    gc.plan(Hq, run.k_pool, run.v_pool, run.batch, ws)
+    outs = []
+    for _ in range(2):
+        out = torch.full((T, Hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+        lse = torch.full((T, Hq), float("nan"), dtype=torch.float32, device="cuda")
+        gc.run_fp8(run.q, run.k_pool, run.v_pool, run.batch, w.scale, ks, vs, ws, out=out, lse=lse)
+        torch.cuda.synchronize()
+        outs.append(H.from_dev_bits(out))
+        assert not ws[QUEUE_BYTES[0]:QUEUE_BYTES[1]].any().item()
+    assert np.array_equal(outs[0], outs[1])
+    rows = H.sample_rows(w, seed=50 + D)
+    ref_out, ref_lse = H.oracle_rows_fp8(run, kref, vref, rows=rows)
+    info = H.compare_attention(w, out, lse, ref_out, ref_lse, rows=rows, contract=True,
+                               vmax=H.e4m3_vmax(vref, vs))
+    say(f"8-bit resident launch, d {D}: {info}")
