@@ -180,7 +180,7 @@ def auto_kernel_name(w, cus, fp8):
     rows = int(w.new_lens.sum()) * g
     grid = units * w.num_kv_heads
     wide = rows * 100 >= units * 256 * 85 and not (cus < grid < 2 * cus)
-    if wide and cus % 8 == 0 and wide_items(w, cus) * w.num_kv_heads >= 4 * cus:
+    if wide and cus % 8 == 0 and wide_items(w, cus) * w.num_kv_heads >= 2 * cus:
         # resident launch: one workgroup per CU taking the items from per-XCD queues
         return f"attention_resident_kernel<{D}{f}> (+ split merge when the plan splits)"
     return f"attention_kernel<{D}, {8 if wide else 4}{f}> (+ split merge when the plan splits)"

@@ -273,16 +273,16 @@ gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& s
     return gc::launch_plan(plan_args(geo, b, sh, pl, ws), stream) == hipSuccess ? GC_OK : GC_ERR_HIP;
 }
 
-// Wide tiles with at least four rounds of work items per compute unit
-// run as a resident launch (one workgroup per CU taking items from per-XCD queues;
+// Wide tiles with at least two rounds of work items per compute unit run as a
+// resident launch (one workgroup per CU taking items from per-XCD queues;
 // attention.hip): it removes the dispatch gaps between items and lets the XCDs that
-// finish first take the last items of the others. With fewer rounds the tickets cost
-// more than they save. 0: the regular launch.
+// finish first take the last items of the others. A single round has nothing to
+// balance. 0: the regular launch.
 int resident_workgroups(const gc_geometry* geo, const Shape& sh, const Plan& pl) {
     if (!sh.wide) return 0;
     const int cus = device_cus();
     if (cus % gc::kQueues != 0) return 0;
-    return pl.items * geo->num_kv_heads >= 4LL * cus ? cus : 0;
+    return pl.items * geo->num_kv_heads >= 2LL * cus ? cus : 0;
 }
 
 // Pools of bf16 elements (fp8 false, scales 1) or of E4M3 codes with one scale each.
