@@ -24,7 +24,7 @@ def bits(t):
     return t.view(torch.int16 if t.element_size() == 2 else torch.int32).cpu().numpy()
 
 
-def one_case(w, split):
+def one_case(w, split, rows=None):
     import torch
     import paper_2505_23970_amd as gc
     say(f"no-alloc case {w.name}: B={w.batch} T={w.total_new} split={split}")
@@ -42,8 +42,8 @@ def one_case(w, split):
     assert np.array_equal(bits(out_a), bits(out_b))
     assert np.array_equal(bits(lse_a), bits(lse_b))
     kp, vp = H.oracle_pools(w)
-    ref, ref_lse = H.oracle_rows(w, kp, vp)
-    H.compare_attention(w, out_b, lse_b, ref, ref_lse)
+    ref, ref_lse = H.oracle_rows(w, kp, vp, rows=rows)
+    H.compare_attention(w, out_b, lse_b, ref, ref_lse, rows=rows)
 
 
 @pytest.mark.parametrize("split", [None, 2])
@@ -55,6 +55,20 @@ def test_noalloc_two_calls_second_smaller(split):
     small = W.build([40, 7], [9, 30], 16, 2, 128, seed=401, name="noalloc_small")
     one_case(big, split)
     one_case(small, split)
+
+
+def test_noalloc_resident_launch_two_calls_second_smaller():
+    """Batches large enough for the resident wide-tile launch (its work queues live in
+    the static scratch too): two calls, the second smaller, each bitwise equal to the
+    workspace call; sampled rows against the oracle."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    big = W.build([0, 0, 0, 0, 2000, 3000], [1024, 1024, 1024, 1024, 200, 100], 64, 8, 128, seed=403,
+                  name="noalloc_resident_big")
+    small = W.build([0, 0, 0, 1500], [1024, 1024, 1024, 100], 64, 8, 128, seed=404, name="noalloc_resident_small")
+    one_case(big, None, rows=H.sample_rows(big, seed=61))
+    one_case(small, None, rows=H.sample_rows(small, seed=62))
 
 
 def test_noalloc_rejects_a_batch_beyond_its_scratch():
