@@ -166,15 +166,17 @@ V_SCALE_FP8 = 0.0213
 
 
 def auto_kernel_name(w, cus, fp8):
-    """Kernel the library's automatic tiling picks for w (the rule of choose_tiling in
-    the C ABI, restated: small tiles when every request has n * g <= 16, else wide
-    tiles when 256-row tiles are >= 85 % full and their grid is not between one and
-    two per compute unit, else 128-row tiles)."""
+    """Kernel the library's automatic tiling picks for w, named as in the kernel trace
+    (the rule of choose_tiling and resident_workgroups in the C ABI, restated: small
+    tiles when every request has n * g <= 16, else wide tiles when 256-row tiles are
+    >= 85 % full and their grid is not between one and two per compute unit, run as a
+    resident launch from two rounds of work items on, else 128-row tiles)."""
     g = w.num_q_heads // w.num_kv_heads
     D = w.head_dim
-    f = ", fp8" if fp8 else ""
+    f = "true" if fp8 else "false"
+    split = " (+ split merge when the plan splits)"
     if g <= 16 and int(w.new_lens.max()) * g <= 16:
-        return f"attention_small_kernel<{D}{f}> (+ split merge when the plan splits)"
+        return f"attention_small_kernel<{D}, {f}>" + split
     tq = 256 // g
     units = int(sum((int(n) + tq - 1) // tq for n in w.new_lens))
     rows = int(w.new_lens.sum()) * g
@@ -182,8 +184,8 @@ def auto_kernel_name(w, cus, fp8):
     wide = rows * 100 >= units * 256 * 85 and not (cus < grid < 2 * cus)
     if wide and cus % 8 == 0 and wide_items(w, cus) * w.num_kv_heads >= 2 * cus:
         # resident launch: one workgroup per CU taking the items from per-XCD queues
-        return f"attention_resident_kernel<{D}{f}> (+ split merge when the plan splits)"
-    return f"attention_kernel<{D}, {8 if wide else 4}{f}> (+ split merge when the plan splits)"
+        return f"attention_resident_kernel<{D}, {f}>" + split
+    return f"attention_kernel<{D}, {8 if wide else 4}, {f}>" + split
 
 
 def wide_items(w, cus):

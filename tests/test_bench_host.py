@@ -7,6 +7,7 @@ import subprocess
 import sys
 
 import numpy as np
+import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
@@ -90,3 +91,17 @@ def test_every_bench_workload_is_well_formed():
         assert w.flops() > 0 and w.attn_bytes() > 0
         assert np.all(w.prefix_lens >= 0) and np.all(w.new_lens >= 0)
         assert w.q.shape == (w.total_new, w.num_q_heads, w.head_dim)
+
+
+@pytest.mark.parametrize("name,fp8", [("mixed_hit_miss_70b", False), ("llama3_70b_chat", False),
+                                      ("long_reuse_70b", False), ("long_reuse_70b_n16", False),
+                                      ("llama3_8b", False), ("llama3_8b", True), ("decode_70b", False),
+                                      ("decode_70b", True)])
+def test_named_kernel_is_the_profiled_one(name, fp8):
+    """bench.py names the kernel the library picks by restating its host rules; the
+    committed profile of the workload records the kernel the GPU actually ran."""
+    path = os.path.join(ROOT, "profiles", f"attention_{name}{'_fp8' if fp8 else ''}.md")
+    first = open(path).readline()
+    profiled = first[2:].split(" \u2014 ")[0].strip()
+    w = bench.WORKLOADS[name]()
+    assert bench.auto_kernel_name(w, 256, fp8).startswith(profiled + " "), (profiled, first)
