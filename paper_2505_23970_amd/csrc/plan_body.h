@@ -14,7 +14,8 @@
 //   3. every item is written straight to its sorted position (an LDS cursor per
 //      cost bucket, advanced once per distinct chunk size of a tile); split query
 //      tiles take their partial slots and merge entry from two LDS counters.
-// The hardware dispatcher starts workgroups in index order: the items of the
+// The hardware dispatcher starts workgroups in index order (the resident launch
+// hands out its tickets in the same order): the items of the
 // longest requests start first, each request's items together, and the launch
 // ends on its lightest items in cost order (longest-processing-time scheduling
 // where it matters, at the end). Order inside a bucket and slot numbers may
