@@ -247,11 +247,15 @@ def measured_mfma_tflops(iterations=4000, reps=5):
 
 
 def traffic_sources(kernel_source):
-    """Sources that decide an attention launch's memory traffic: the kernel's file, the
-    planner that orders its work items and the host policy that picks the tiling,
-    key split and order (and the shared definitions)."""
-    return [kernel_source, "paper_2505_23970_amd/csrc/plan_body.h", "paper_2505_23970_amd/csrc/api.hip",
-            "paper_2505_23970_amd/csrc/gc_internal.h"]
+    """Sources that decide an attention launch's memory traffic: the file that launches
+    the kernel (with the kernel's own file where that is another), the planner that
+    orders its work items, the host policy that picks the tiling, key split and order,
+    the shared definitions and the build script (its flags)."""
+    csrc = "paper_2505_23970_amd/csrc/"
+    own = [kernel_source]
+    if kernel_source in (csrc + "attention.hip", csrc + "attention_plain.hip"):
+        own.append(csrc + "attention_kernels.h")
+    return own + [csrc + "plan_body.h", csrc + "api.hip", csrc + "gc_internal.h", "paper_2505_23970_amd/build.py"]
 
 
 def code_text(text):

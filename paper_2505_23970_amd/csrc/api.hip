@@ -275,7 +275,7 @@ gc_status enqueue_plan(const gc_geometry* geo, const gc_batch* b, const Shape& s
 
 // Wide tiles with at least two rounds of work items per compute unit run as a
 // resident launch (one workgroup per CU taking items from per-XCD queues;
-// attention.hip): it removes the dispatch gaps between items and lets the XCDs that
+// attention_kernels.h): it removes the dispatch gaps between items and lets the XCDs that
 // finish first take the last items of the others. A single round has nothing to
 // balance. 0: the regular launch.
 int resident_workgroups(const gc_geometry* geo, const Shape& sh, const Plan& pl) {

@@ -219,6 +219,9 @@ hipError_t launch_prepare(const AppendArgs& aa, const PlanArgs& pa, int head_dim
 // the items from the work queues instead of one workgroup per item
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, bool fp8,
                             int resident, hipStream_t s);
+// the same over 8-bit pools (launch_attention forwards fp8 launches here)
+hipError_t launch_attention_fp8(const AttnArgs& a, int head_dim, int64_t num_items, bool wide, int resident,
+                                hipStream_t s);
 // attention with the KV append fused in (AttnArgs with k_new, v_new, k_dst, v_dst
 // set); prefill tiles over bf16 pools
 hipError_t launch_attention_append(const AttnArgs& a, int head_dim, int64_t num_items, bool wide,
