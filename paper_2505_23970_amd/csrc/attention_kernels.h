@@ -354,6 +354,9 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a, const unsigned
     // for the next tile occupy registers during the products; five for bf16 pools at
     // d = 128, measured 0.6-2 % faster than six on the long-prefix workloads)
     constexpr int kAhead = (!FP8 && !FUSE && D == 128) ? 5 : ((FP8 || FUSE) && WAVES == 4 && D == 128) ? 4 : 6;
+    // (value fragments: four on the 8-wavefront bf16 tiles at d = 128, where the weights
+    // computed between the PV products keep the wavefront busy meanwhile)
+    constexpr int kAheadV = (!FP8 && !FUSE && D == 128 && WAVES == 8) ? 4 : kAhead;
     // hook(i) runs after the i-th QK^T product is issued (the next tile's copies go there)
     auto compute_tile = [&](const unsigned char* kb, const unsigned char* vb, int kt, auto&& hook) {
         // S^T = K_tile . Q^T: MFMA i uses K fragment (k = i/2, block b = i%2). Every
@@ -383,7 +386,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a, const unsigned
             vf[i] = *reinterpret_cast<const bf16x8*>(vb + st * kPageBytes + d * 32 + ((hh ^ ((d >> 3) & 1)) * 16));
         };
 #pragma unroll
-        for (int i = 0; i < kAhead; ++i) vread(i);
+        for (int i = 0; i < kAheadV; ++i) vread(i);
         __builtin_amdgcn_sched_barrier(0);
 
         // s[b][e] is the score of tile key 32b + 16(e>>3) + 8hh + (e&7)
@@ -459,7 +462,7 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a, const unsigned
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
                 const int i = st * DB + db;
-                if (i + kAhead < 4 * DB) vread(i + kAhead);
+                if (i + kAheadV < 4 * DB) vread(i + kAheadV);
                 o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], pf[st], o[db], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
                 if (st + 1 < 4 && (db + 1) % (DB / kParts) == 0) {
