@@ -438,8 +438,9 @@ __device__ __forceinline__ void attention_body(const AttnArgs& a, const unsigned
         bf16x8 pf[4];
         constexpr int kParts = (!FP8 && WAVES == 8 && DB >= 4) ? 4 : 2;
         static_assert(DB % kParts == 0 && 4 % kParts == 0, "weight parts");
-        // weights p, p + 1 of step st as bf16, and their sums: pair q of the step (2q, 2q + 1)
-        // goes to l_run for even q, l_run1 for odd q, in pair order
+        // part `part` of step st's eight weights, as bf16, and their row sums: pair q of the
+        // step (weights 2q, 2q + 1) goes to l_run for even q and to l_run1 for odd q, in pair
+        // order, so the sums do not depend on kParts
         auto weights_part = [&](int st, int part) {
             const int b = st >> 1, e0 = (st & 1) * 8;
 #pragma unroll
